@@ -1,0 +1,260 @@
+"""Benchmark: PAT reduce-scatter of 128 virtual ranks on one MI355X.
+
+Workload (the bandwidth-roofline case): reduce-scatter (sum), N = 128
+virtual ranks, bf16 inputs N(0,1) from seed 0x5041545, float32 partial sums,
+a 4 MiB output chunk (2,097,152 bf16) per rank -- 64 GiB of rank send buffers
+resident in HBM.  One "step" = one whole reduce-scatter over all 128 ranks.
+
+Prints one JSON line:
+* value      -- aggregate bus bandwidth, N * (N-1) * C / t  (nccl-tests busBW
+                summed over the N virtual ranks; the per-rank figure is
+                bus_gbps_per_rank)
+* roofline   -- algorithmic memory bytes of the dominant kernel per launch /
+                its average launch duration (HIP events on its stream), against
+                the 8 TB/s HBM3E peak; traffic from the committed rocprofv3
+                counter summary when it matches the current kernel source
+* cpu_baseline -- the CPU oracle (numpy, executing the PAT steps) timed on
+                a bounded sample of the same workload, in the same unit
+
+python bench.py [--steps K] [--warmup W] [--mode persistent|graph|stream]
+                [--workload 1..5] [--cpu-seconds S] [--no-cpu-baseline]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "bus GB/s and % of HBM peak for PAT AG/RS; small-size latency µs"
+
+WORKLOADS = {
+    # id: (collective, N, count, dtype, distribution, seed, description)
+    1: ("rs", 6, 1024, "int32", "int32_pm2p20", 0x5041541,
+        "PAT reduce-scatter (sum), N=6 virtual ranks, int32 U[-2^20,2^20], 1024-element output chunk"),
+    2: ("ag", 24, 32768, "bfloat16", "bf16_normal", 0x5041542,
+        "PAT all-gather, N=24 virtual ranks, bf16 N(0,1), 32768-element (64 KiB) chunk per rank"),
+    3: ("rs", 64, 262144, "float32", "f32_normal", 0x5041543,
+        "PAT reduce-scatter (sum), N=64 virtual ranks, fp32 N(0,1), 262144-element (1 MiB) output chunk"),
+    4: ("rs", 1000, 64, "float32", "f32_pm1", 0x5041544,
+        "PAT reduce-scatter (sum), N=1000 virtual ranks, fp32 U[-1,1), 64-element (256 B) output chunk"),
+    5: ("rs", 128, 2097152, "bfloat16", "bf16_normal", 0x5041545,
+        "PAT reduce-scatter (sum), N=128 virtual ranks, bf16 N(0,1) in / fp32 accumulation, "
+        "2097152-element (4 MiB) output chunk per rank, 64 GiB of rank buffers in HBM"),
+}
+
+KERNEL_SOURCES = ["paper_2506_20252_amd/csrc/kernels.hip", "paper_2506_20252_amd/csrc/kernels.hpp",
+                  "paper_2506_20252_amd/csrc/device_types.hpp"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload_id, mode):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_workload{workload_id}_{mode}.txt")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_source_hash:\s*(\w+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(wid, target_seconds, sample_inputs, m_cap):
+    """Time the oracle on a bounded sample: every destination chunk, the first
+    m element positions of each, m calibrated so the run takes ~target.
+
+    sample_inputs(m) returns the workload's inputs at those positions."""
+    import numpy as np  # noqa: F401
+
+    from oracle import pat as opat
+
+    coll, n, count, dtype, dist, seed, _ = WORKLOADS[wid]
+    esize = 2 if dtype == "bfloat16" else 4
+
+    def run(x):
+        if coll == "rs":
+            t = opat.aggregation_level(n, count * 4, 8 << 20)
+            t0 = time.perf_counter()
+            opat.reducescatter(x, t, dtype)
+        else:
+            t = opat.aggregation_level(n, count * esize, 8 << 20)
+            t0 = time.perf_counter()
+            opat.allgather(x, t)
+        return time.perf_counter() - t0
+
+    m = min(count, m_cap, 2048)
+    elapsed = run(sample_inputs(m))
+    if m < count:
+        m = int(min(count, m_cap, max(m, m * target_seconds / max(elapsed, 1e-3))))
+        elapsed = run(sample_inputs(m))
+    bus_bytes = float(n) * (n - 1) * m * esize
+    return {"value": bus_bytes / elapsed / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {n} destination chunks x the first {m} of {count} element positions "
+                      f"({m / count:.3g} of the operation); numpy, one thread; {elapsed:.1f} s",
+            "seconds": round(elapsed, 2)}
+
+
+def copy_probe(nbytes, reps):
+    """A plain device-to-device copy of known size: reads and writes nbytes."""
+    import torch
+    n = nbytes // 2
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_bytes": 2 * n, "read_bytes": 2 * n, "write_bytes": 2 * n, "ms": round(ms, 4),
+                      "GBps_read_plus_write": round(4 * n / ms / 1e6, 1)}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--mode", default="graph", choices=["persistent", "graph", "stream"])
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="instead: time a plain device copy of BYTES (the achievable-bandwidth line, and "
+                         "the calibration kernel for the memory-traffic counters)")
+    ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: all virtual ranks are emulated on one GPU; runs on more than one GPU "
+              "are not supported (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe, args.steps)
+        return
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    coll, n, count, dtype, dist, seed, desc = WORKLOADS[args.workload]
+    tdt = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}[dtype]
+    esize = 2 if dtype == "bfloat16" else 4
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    pat.lib()
+    pat.check(pat.pat_set_exec_mode(args.mode))
+
+    if coll == "rs":
+        send = torch.empty((n, n * count), dtype=tdt, device=dev)
+        recv = torch.empty((n, count), dtype=tdt, device=dev)
+        code = pat.PAT_REDUCESCATTER
+    else:
+        send = torch.empty((n, count), dtype=tdt, device=dev)
+        recv = torch.empty((n, n * count), dtype=tdt, device=dev)
+        code = pat.PAT_ALLGATHER
+    for x in range(n):
+        synth.fill(send[x], dist, seed, x)
+    sends, recvs = list(send), list(recv)
+    torch.cuda.synchronize()
+
+    st, info = pat.pat_plan_info(code, n, count, dtype)
+    pat.check(st)
+
+    def op():
+        if coll == "rs":
+            return pat.pat_reducescatter(sends, recvs, count, dtype, pat.PAT_SUM, n, stream)
+        return pat.pat_allgather(sends, recvs, count, dtype, n, stream)
+
+    for _ in range(args.warmup):
+        pat.check(op(), "warmup")
+    torch.cuda.synchronize()
+    pat.check(pat.pat_check_device_status(stream))
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        pat.check(op(), "timed")
+    end.record(stream)
+    torch.cuda.synchronize()
+    pat.check(pat.pat_check_device_status(stream))
+    ms = start.elapsed_time(end) / args.steps
+    sec = ms / 1e3
+
+    bus_per_rank = info["bus_bytes_per_rank"]
+    launches = 1 if args.mode == "persistent" else info["steps"] * info["pieces"]
+    alg_per_launch = info["alg_bytes"] / launches
+    launch_sec = sec / launches
+    achieved = alg_per_launch / launch_sec / 1e9
+    traffic = committed_traffic(args.workload, args.mode)
+    kernel = ("persistent_kernel" if args.mode == "persistent" else "step_kernel") + \
+        ("<reduce-scatter>" if coll == "rs" else "<all-gather>")
+
+    out = {
+        "metric": METRIC,
+        "value": round(n * bus_per_rank / sec / 1e9, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if coll == "rs" and dtype != "int32" else ("int32" if dtype == "int32" else "bytes"),
+        "data": "synthetic",
+        "config": {"workload": desc, "nranks": n, "count": count, "input_dtype": dtype,
+                   "collective": "reduce-scatter" if coll == "rs" else "all-gather", "exec_mode": args.mode,
+                   "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
+                   "pat_steps": info["steps"], "pieces": info["pieces"], "seed": seed},
+        "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),
+        "latency_us": round(ms * 1e3, 2),
+        "alg_bytes_per_op": info["alg_bytes"],
+        "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4),
+        "roofline": {"bound": "hbm", "kernel": kernel, "launches_per_op": launches,
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        # The oracle's inputs: the first m positions of every chunk of the
+        # generator-filled send buffers (the collective only reads them).
+        import numpy as np
+
+        def sample_inputs(m):
+            view = send.view(n, n, count) if coll == "rs" else send
+            part = view[..., :m].contiguous()
+            if dtype == "bfloat16":
+                return part.view(torch.int16).cpu().numpy().view(np.uint16)
+            return part.cpu().numpy()
+
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds, sample_inputs, min(count, 1 << 20))
+    del send, recv, sends, recvs
+    torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

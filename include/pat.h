@@ -1,0 +1,196 @@
+/*
+ * pat.h -- C-ABI of the PAT (Parallel Aggregated Trees) all-gather and
+ * reduce-scatter library for AMD Instinct MI355X (gfx950).
+ *
+ * Operations follow S. Jeaugey, "PAT: a new algorithm for all-gather and
+ * reduce-scatter operations at scale" (arXiv:2506.20252):
+ *   - the operations and their buffer rules: section "All-gather and
+ *     reduce-scatter algorithms" (MPI semantics: the send buffer is never
+ *     written; the reduce-scatter receive buffer is small);
+ *   - the algorithm: sections "Binomial-tree based algorithms" (shifted
+ *     binomial trees, farthest dimension first, truncated trees for any rank
+ *     count), "The PAT algorithm" (intermediate buffers of bounded size,
+ *     aggregation limited to T parallel sub-trees, far-first linear schedule)
+ *     and "Conversion to reduce-scatter operations" (reversed trees, close
+ *     dimensions first, accumulation buffers).
+ *
+ * One GPU emulates N virtual ranks.  Every rank's send buffer, receive buffer
+ * and intermediate buffers ("slots") live in this GPU's memory, and each
+ * network transfer of the paper is a device-local copy into the receiving
+ * rank's slot or receive buffer.  Nothing crosses between GPUs.
+ *
+ * Conventions for every entry point:
+ *   - Status codes only; nothing is thrown across this boundary.
+ *   - `sendbufs` / `recvbufs` are HOST arrays of `nranks` DEVICE pointers,
+ *     read during the call only (the library copies them into a device
+ *     table it owns).  The buffers themselves are owned by the caller and
+ *     must stay valid until `stream` has finished the operation.
+ *   - Calls are asynchronous with respect to the host and ordered on
+ *     `stream`.  Calls that use the same (operation, nranks, count, dtype,
+ *     buffer budget) share library-owned intermediate buffers: they must be
+ *     ordered on one stream (or otherwise serialised by the caller).
+ *   - Pointers must be aligned to the element size.  When every pointer is
+ *     16-byte aligned and count * sizeof(element) is a multiple of 16, the
+ *     kernels move 128-bit vectors; otherwise they move single elements
+ *     (correct, slower).
+ *   - In place is allowed only in the MPI/NCCL form given per operation;
+ *     any other overlap between a receive buffer and another buffer is
+ *     PAT_ERR_INVALID_ARGUMENT.  Send buffers may overlap each other.
+ *   - The library is thread-safe; plans are cached per device.
+ */
+#ifndef PAT_H_
+#define PAT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PAT_OK = 0,
+  PAT_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, alignment or overlap */
+  PAT_ERR_UNSUPPORTED = 2,      /* dtype / op / mode not provided */
+  PAT_ERR_OUT_OF_MEMORY = 3,    /* intermediate buffers could not be allocated */
+  PAT_ERR_HIP = 4,              /* a HIP runtime call failed; see pat_last_hip_error() */
+  PAT_ERR_TIMEOUT = 5,          /* a persistent kernel's step barrier gave up waiting */
+  PAT_ERR_INTERNAL = 6          /* a plan failed its own consistency checks */
+} pat_status_t;
+
+typedef enum {
+  PAT_INT32 = 0,   /* reduce-scatter sums wrap modulo 2^32 */
+  PAT_FLOAT32 = 1, /* IEEE float32 adds, round to nearest even */
+  PAT_BFLOAT16 = 2 /* reduce-scatter: partial sums carried in float32, rounded
+                      to bfloat16 (nearest even) once, at the owning rank */
+} pat_dtype_t;
+
+typedef enum { PAT_SUM = 0 } pat_op_t;
+
+typedef enum {
+  PAT_ALLGATHER = 0,
+  PAT_REDUCESCATTER = 1
+} pat_collective_t;
+
+typedef enum {
+  /* One cooperative launch per operation; a device-wide barrier separates
+   * the steps.  Its grid is capped at 2 workgroups per compute unit
+   * (PAT_PERSISTENT_BLOCKS_PER_CU overrides) so that it is co-resident. */
+  PAT_EXEC_PERSISTENT = 0,
+  /* One kernel per step, captured once per plan (and vector width) into a
+   * HIP graph and replayed.  The default. */
+  PAT_EXEC_GRAPH = 1,
+  /* One kernel per step, launched directly on the stream. */
+  PAT_EXEC_STREAM = 2
+} pat_exec_mode_t;
+
+/*
+ * All-gather (section "All-gather and reduce-scatter algorithms"):
+ *   recvbufs[r][x * count + i] = sendbufs[x][i]   for all ranks r, x and i < count.
+ *   sendbufs[x]: `count` elements.   recvbufs[r]: nranks * count elements.
+ * Steps: the all-gather steps of section "The PAT algorithm".
+ * In place: sendbufs[r] == recvbufs[r] + r * count (the own chunk is then not copied).
+ * count == 0: PAT_OK, nothing is launched.  nranks == 1: a plain copy.
+ */
+pat_status_t pat_allgather(const void* const* sendbufs, void* const* recvbufs, size_t count,
+                           pat_dtype_t dtype, int nranks, hipStream_t stream);
+
+/*
+ * Reduce-scatter, sum (sections "All-gather and reduce-scatter algorithms" and
+ * "Conversion to reduce-scatter operations"):
+ *   recvbufs[R][i] = sum over x of sendbufs[x][R * count + i]   for i < count.
+ *   sendbufs[x]: nranks * count elements.   recvbufs[R]: `count` elements.
+ * Summation order: the reversed binomial tree of chunk R rooted at rank R,
+ * children added nearest first; it does not depend on the buffer budget.
+ * In place: recvbufs[r] == sendbufs[r] + r * count.
+ * count == 0: PAT_OK, nothing is launched.  nranks == 1: a plain copy.
+ */
+pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbufs, size_t count,
+                               pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream);
+
+/*
+ * Intermediate-buffer budget B, in bytes per slot (section "The PAT
+ * algorithm": the aggregation is limited to what the buffer holds).  A rank
+ * holds at most ceil(log2 nranks) slots of at most B bytes each.  The plan
+ * uses T = 2^t parallel sub-trees, the largest power of two <= 2^(L-1) whose
+ * largest step fits B; a chunk larger than B is processed in pieces of at
+ * most B bytes.  0 restores the default (8 MiB, or the PAT_BUFFER_BYTES
+ * environment variable).  Affects plans created afterwards.
+ */
+pat_status_t pat_set_buffer_bytes(size_t bytes_per_slot);
+size_t pat_get_buffer_bytes(void);
+
+/* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_GRAPH, or the
+ * PAT_EXEC_MODE environment variable (persistent | graph | stream). */
+pat_status_t pat_set_exec_mode(int mode);
+int pat_get_exec_mode(void);
+
+/* Wall-clock limit of one wait at the persistent kernel's step barrier, in
+ * microseconds (0 = default, 10 s).  When exceeded the kernel records a
+ * timeout (see pat_check_device_status) and exits instead of waiting forever;
+ * the operation's result is then undefined. */
+pat_status_t pat_set_barrier_timeout_us(uint32_t microseconds);
+
+/* Plan summary.  Host-only: needs no GPU. */
+typedef struct {
+  int nranks;
+  int L;                      /* ceil(log2 nranks) */
+  int t;                      /* T = 2^t parallel sub-trees */
+  int T;
+  int steps;                  /* communication steps per piece */
+  int pieces;                 /* pieces a chunk is split into (1 unless chunk > budget) */
+  int max_chunks_per_step;    /* largest number of chunks a rank sends in one step */
+  int vector_path;            /* 1: 128-bit kernels possible for aligned pointers */
+  size_t count;               /* elements per chunk */
+  size_t piece_elems;         /* elements per piece */
+  size_t slot_elem_bytes;     /* 4 for bf16 reduce-scatter (float32 partials) */
+  int slot_dims;              /* distinct slot dimensions a rank uses */
+  int slot_chunks_per_rank;   /* chunk-sized slot entries per rank */
+  size_t slot_bytes_per_rank; /* intermediate memory per rank */
+  size_t slot_bytes_total;    /* all ranks, plus the float32 root accumulators */
+  double alg_bytes;           /* memory bytes the steps must read + write per operation */
+  double bus_bytes_per_rank;  /* (nranks - 1) * count * sizeof(dtype) */
+} pat_plan_info_t;
+
+pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,
+                           pat_plan_info_t* out);
+
+/*
+ * Step table of a plan (one piece), host-only.  For step s (in execution
+ * order) step_d[s] is the distance d and step_k[s] the number of chunks each
+ * rank handles; the entries of step s follow those of step s-1.  Entry j:
+ *   pos[j]   tree position p (all-gather: the sender; reduce-scatter: the receiver);
+ *   a[j], b[j], c[j]  slot indices (chunk entries of a rank's slot area) or markers:
+ *     all-gather:     a = source slot or -1 (own send buffer),
+ *                     b = slot written at the receiver or -1 (receive buffer only);
+ *     reduce-scatter: a = child's slot or -1 (child's raw input),
+ *                     b = own accumulator slot, -1 (own raw input), -2 (root accumulator),
+ *                     c = destination slot, -2 (root accumulator), -3 (root, last receive).
+ * Arrays must hold max_steps / max_entries elements; *nsteps / *nentries get
+ * the sizes (PAT_ERR_INVALID_ARGUMENT if they do not fit).
+ */
+pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,
+                            int32_t* step_d, int32_t* step_k, int max_steps, int32_t* pos,
+                            int32_t* a, int32_t* b, int32_t* c, int max_entries, int* nsteps,
+                            int* nentries);
+
+/* Waits for `stream`, then reports (and clears) a barrier timeout recorded by
+ * a persistent kernel on the current device: PAT_OK or PAT_ERR_TIMEOUT. */
+pat_status_t pat_check_device_status(hipStream_t stream);
+
+/* Last hipError_t seen by a call that returned PAT_ERR_HIP (0 if none). */
+int pat_last_hip_error(void);
+
+const char* pat_status_string(pat_status_t status);
+
+/* Frees every plan, intermediate buffer and graph on every device.  Waits for
+ * the devices first.  Later calls rebuild what they need. */
+pat_status_t pat_finalize(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAT_H_ */

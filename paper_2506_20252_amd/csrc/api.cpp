@@ -1,0 +1,549 @@
+// C-ABI of the PAT library: argument checks, plan cache, execution modes.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <tuple>
+#include <vector>
+
+#include "../../include/pat.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace {
+
+constexpr size_t kDefaultBudget = size_t(8) << 20;
+constexpr uint32_t kDefaultTimeoutUs = 10u * 1000u * 1000u;
+constexpr int kMaxRanks = 1 << 16;
+
+std::mutex g_mu;
+size_t g_budget = 0;     // 0: default
+int g_mode = -1;         // -1: environment / default
+uint32_t g_timeout_us = 0;  // 0: default
+std::atomic<int> g_last_hip{0};
+
+size_t budget_now() {
+  if (g_budget) return g_budget;
+  if (const char* e = std::getenv("PAT_BUFFER_BYTES")) {
+    const long long v = std::atoll(e);
+    if (v > 0) return size_t(v);
+  }
+  return kDefaultBudget;
+}
+
+int mode_now() {
+  if (g_mode >= 0) return g_mode;
+  if (const char* e = std::getenv("PAT_EXEC_MODE")) {
+    if (!std::strcmp(e, "persistent")) return PAT_EXEC_PERSISTENT;
+    if (!std::strcmp(e, "stream")) return PAT_EXEC_STREAM;
+  }
+  return PAT_EXEC_GRAPH;
+}
+
+uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }
+
+// Persistent grid: at most this many workgroups per compute unit.  The
+// occupancy calculator's figure (7 per CU for these kernels on MI355X) was
+// not co-resident in practice -- the barrier timed out -- while up to 4 per
+// CU was; 2 leaves a wide margin.  0 means "the calculator's figure".
+int blocks_per_cu_cap() {
+  if (const char* e = std::getenv("PAT_PERSISTENT_BLOCKS_PER_CU")) return std::max(0, std::atoi(e));
+  return 2;
+}
+
+int elem_size(pat_dtype_t t) { return t == PAT_BFLOAT16 ? 2 : 4; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+#define HIP_TRY(expr)                                 \
+  do {                                                \
+    hipError_t e_ = (expr);                           \
+    if (e_ != hipSuccess) {                           \
+      g_last_hip.store((int)e_);                      \
+      return PAT_ERR_HIP;                             \
+    }                                                 \
+  } while (0)
+
+struct Plan {
+  pat::PlanDesc desc;
+  int device = 0;
+  bool has_vec = false;
+  std::vector<pat::DevStep> steps[2];  // [0] element path, [1] 128-bit path
+  pat::DevEntry* d_entries = nullptr;
+  pat::DevStep* d_steps[2] = {nullptr, nullptr};
+  const void** d_send = nullptr;
+  void** d_recv = nullptr;
+  char* d_slots = nullptr;
+  char* d_rootacc = nullptr;
+  unsigned* d_sync = nullptr;  // [0..1] barrier counters, [2] status
+  int64_t slot_chunk_stride = 0, slot_rank_stride = 0, rootacc_stride = 0;
+  std::vector<const void*> h_send;
+  std::vector<void*> h_recv;
+  void** pinned = nullptr;  // 2N pointers staged for upload
+  hipEvent_t upload_done = nullptr;
+  bool upload_pending = false;
+  hipGraphExec_t graph[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};  // [vec][own_copy]
+  int capacity[pat::kNumVariants] = {};
+  int cus = 0;
+  int64_t clock_khz = 0;
+
+  ~Plan() {
+    for (auto& row : graph)
+      for (auto& g : row)
+        if (g) (void)hipGraphExecDestroy(g);
+    if (upload_done) (void)hipEventDestroy(upload_done);
+    if (pinned) (void)hipHostFree(pinned);
+    (void)hipFree(d_entries);
+    (void)hipFree(d_steps[0]);
+    (void)hipFree(d_steps[1]);
+    (void)hipFree(d_send);
+    (void)hipFree(d_recv);
+    (void)hipFree(d_slots);
+    (void)hipFree(d_rootacc);
+    (void)hipFree(d_sync);
+  }
+};
+
+using PlanKey = std::tuple<int, int, int64_t, int, size_t, int>;  // coll, N, count, dtype, budget, device
+std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
+
+// Launch-level steps for one vector width: every schedule step of every piece.
+bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, std::vector<pat::DevStep>* out) {
+  out->clear();
+  for (int piece = 0; piece < d.pieces; ++piece) {
+    const int64_t e0 = int64_t(piece) * d.piece_elems;
+    const int64_t len = std::min<int64_t>(d.piece_elems, d.count - e0);
+    const int64_t bytes = len * d.esize_in;
+    if (bytes % in_bytes) return false;
+    const int64_t V = bytes / in_bytes;
+    for (size_t j = 0; j < d.exec.size(); ++j) {
+      const auto& st = d.exec[j];
+      pat::DevStep ds{};
+      ds.d = st.d;
+      ds.k = st.k;
+      ds.entry0 = st.first;
+      ds.first = j == 0 ? 1 : 0;
+      ds.e0 = e0;
+      ds.V = V;
+      const int64_t edges = int64_t(d.N) * st.k;
+      if (V >= tile) {
+        ds.tiles_per_edge = (V + tile - 1) / tile;
+        ds.items = edges * ds.tiles_per_edge;
+      } else {
+        ds.tiles_per_edge = 0;
+        ds.items = (edges * V + tile - 1) / tile;
+      }
+      out->push_back(ds);
+    }
+  }
+  return true;
+}
+
+pat::Variant variant_for(int coll, pat_dtype_t dt, bool vec) {
+  if (coll == 0) return vec ? pat::kAgVec : (dt == PAT_BFLOAT16 ? pat::kAgS2 : pat::kAgS4);
+  switch (dt) {
+    case PAT_INT32: return vec ? pat::kRsI32Vec : pat::kRsI32S;
+    case PAT_FLOAT32: return vec ? pat::kRsF32Vec : pat::kRsF32S;
+    default: return vec ? pat::kRsB16Vec : pat::kRsB16S;
+  }
+}
+
+pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int device,
+                         Plan** out) {
+  auto p = std::make_unique<Plan>();
+  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, &p->desc)) return PAT_ERR_INVALID_ARGUMENT;
+  pat::PlanDesc& d = p->desc;
+  p->device = device;
+  const bool vec_ok = (count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
+  const pat::Variant vs = variant_for(coll, dt, false), vv = variant_for(coll, dt, true);
+  if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
+  p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
+
+  p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
+  p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
+  if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)round_up(size_t(d.piece_elems) * 4, 256);
+
+  auto alloc = [](void** ptr, size_t bytes) -> pat_status_t {
+    if (bytes == 0) return PAT_OK;
+    hipError_t e = hipMalloc(ptr, bytes);
+    if (e == hipErrorOutOfMemory) {
+      (void)hipGetLastError();
+      return PAT_ERR_OUT_OF_MEMORY;
+    }
+    if (e != hipSuccess) {
+      g_last_hip.store((int)e);
+      return PAT_ERR_HIP;
+    }
+    return PAT_OK;
+  };
+  pat_status_t s;
+  if ((s = alloc((void**)&p->d_entries, d.entries.size() * sizeof(pat::DevEntry))) != PAT_OK) return s;
+  for (int v = 0; v < 2; ++v)
+    if ((s = alloc((void**)&p->d_steps[v], p->steps[v].size() * sizeof(pat::DevStep))) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_send, N * sizeof(void*))) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_recv, N * sizeof(void*))) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_slots, size_t(p->slot_rank_stride) * N)) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_rootacc, size_t(p->rootacc_stride) * N)) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_sync, 4 * sizeof(unsigned))) != PAT_OK) return s;
+  HIP_TRY(hipMemset(p->d_sync, 0, 4 * sizeof(unsigned)));
+  if (const char* e = std::getenv("PAT_POISON_SLOTS")) {
+    if (e[0] == '1') {
+      if (p->d_slots) HIP_TRY(hipMemset(p->d_slots, 0xFF, size_t(p->slot_rank_stride) * N));
+      if (p->d_rootacc) HIP_TRY(hipMemset(p->d_rootacc, 0xFF, size_t(p->rootacc_stride) * N));
+    }
+  }
+  if (!d.entries.empty())
+    HIP_TRY(hipMemcpy(p->d_entries, d.entries.data(), d.entries.size() * sizeof(pat::DevEntry),
+                      hipMemcpyHostToDevice));
+  for (int v = 0; v < 2; ++v)
+    if (!p->steps[v].empty())
+      HIP_TRY(hipMemcpy(p->d_steps[v], p->steps[v].data(), p->steps[v].size() * sizeof(pat::DevStep),
+                        hipMemcpyHostToDevice));
+  HIP_TRY(hipHostMalloc((void**)&p->pinned, 2 * size_t(N) * sizeof(void*), hipHostMallocDefault));
+  HIP_TRY(hipEventCreateWithFlags(&p->upload_done, hipEventDisableTiming));
+  if (const char* e = std::getenv("PAT_DEBUG")) {
+    if (e[0] == '1') {
+      std::fprintf(stderr,
+                   "[pat] plan coll=%d N=%d count=%lld dtype=%d L=%d t=%d T=%d steps=%zu pieces=%d "
+                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d\n",
+                   coll, N, (long long)count, (int)dt, d.sched.L, d.sched.t, d.sched.T, d.exec.size(),
+                   d.pieces, d.max_k, d.slots.entries, (long long)(p->slot_rank_stride * N), d.alg_bytes,
+                   (int)p->has_vec);
+    }
+  }
+  *out = p.get();
+  g_plans[PlanKey(coll, N, count, (int)dt, budget, device)] = std::move(p);
+  return PAT_OK;
+}
+
+// Receive buffers may not overlap anything except the in-place alias of the
+// same rank (all-gather: send inside recv at chunk r; reduce-scatter: recv
+// inside send at chunk r).  Send buffers may overlap each other (read-only).
+bool overlaps_ok(int coll, const void* const* send, void* const* recv, int N, size_t send_bytes,
+                 size_t recv_bytes, size_t chunk_bytes) {
+  struct Iv {
+    uintptr_t lo, hi;
+    int rank;
+  };
+  std::vector<Iv> rv(N);
+  for (int r = 0; r < N; ++r) {
+    const uintptr_t lo = (uintptr_t)recv[r];
+    rv[r] = {lo, lo + recv_bytes, r};
+  }
+  std::sort(rv.begin(), rv.end(), [](const Iv& a, const Iv& b) { return a.lo < b.lo; });
+  for (int i = 1; i < N; ++i)
+    if (rv[i].lo < rv[i - 1].hi) return false;  // equal lengths: adjacent check suffices
+  for (int r = 0; r < N; ++r) {
+    const uintptr_t lo = (uintptr_t)send[r], hi = lo + send_bytes;
+    auto it = std::upper_bound(rv.begin(), rv.end(), lo, [](uintptr_t v, const Iv& a) { return v < a.hi; });
+    for (; it != rv.end() && it->lo < hi; ++it) {
+      if (it->rank != r) return false;
+      const uintptr_t q = (uintptr_t)recv[r];
+      const bool alias = coll == 0 ? (lo == q + uintptr_t(r) * chunk_bytes)
+                                   : (q == lo + uintptr_t(r) * chunk_bytes);
+      if (!alias) return false;
+    }
+  }
+  return true;
+}
+
+pat_status_t run(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt, int N,
+                 hipStream_t stream) {
+  if (N < 1 || N > kMaxRanks || send == nullptr || recv == nullptr) return PAT_ERR_INVALID_ARGUMENT;
+  if (dt != PAT_INT32 && dt != PAT_FLOAT32 && dt != PAT_BFLOAT16) return PAT_ERR_UNSUPPORTED;
+  const size_t es = (size_t)elem_size(dt);
+  if (count > (size_t(1) << 40) / es || (unsigned __int128)count * es * N > ((unsigned __int128)1 << 62))
+    return PAT_ERR_INVALID_ARGUMENT;
+  if (count == 0) return PAT_OK;
+  bool vec = true;
+  for (int r = 0; r < N; ++r) {
+    if (!send[r] || !recv[r]) return PAT_ERR_INVALID_ARGUMENT;
+    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % es) return PAT_ERR_INVALID_ARGUMENT;
+    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % 16) vec = false;
+  }
+  const size_t chunk = count * es;
+  const size_t send_bytes = coll == 0 ? chunk : chunk * N;
+  const size_t recv_bytes = coll == 0 ? chunk * N : chunk;
+  if (!overlaps_ok(coll, send, recv, N, send_bytes, recv_bytes, chunk)) return PAT_ERR_INVALID_ARGUMENT;
+
+  if (N == 1) {
+    if (send[0] != recv[0])
+      HIP_TRY(hipMemcpyAsync(recv[0], send[0], chunk, hipMemcpyDeviceToDevice, stream));
+    return PAT_OK;
+  }
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  const size_t budget = budget_now();
+  Plan* plan = nullptr;
+  auto it = g_plans.find(PlanKey(coll, N, (int64_t)count, (int)dt, budget, device));
+  if (it != g_plans.end()) {
+    plan = it->second.get();
+  } else {
+    const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, device, &plan);
+    if (s != PAT_OK) return s;
+  }
+  vec = vec && plan->has_vec;
+  const int vi = vec ? 1 : 0;
+
+  bool own_copy = false;
+  if (coll == 0)
+    for (int r = 0; r < N && !own_copy; ++r)
+      own_copy = (const char*)send[r] != (const char*)recv[r] + size_t(r) * chunk;
+
+  // Pointer tables: upload only when they changed since the last call.
+  bool same = plan->h_send.size() == size_t(N);
+  for (int r = 0; r < N && same; ++r) same = plan->h_send[r] == send[r] && plan->h_recv[r] == recv[r];
+  if (!same) {
+    if (plan->upload_pending) HIP_TRY(hipEventSynchronize(plan->upload_done));
+    plan->h_send.assign(send, send + N);
+    plan->h_recv.assign(recv, recv + N);
+    std::memcpy(plan->pinned, send, N * sizeof(void*));
+    std::memcpy(plan->pinned + N, recv, N * sizeof(void*));
+    HIP_TRY(hipMemcpyAsync(plan->d_send, plan->pinned, N * sizeof(void*), hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipMemcpyAsync(plan->d_recv, plan->pinned + N, N * sizeof(void*), hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipEventRecord(plan->upload_done, stream));
+    plan->upload_pending = true;
+  }
+
+  const pat::PlanDesc& d = plan->desc;
+  pat::KCtx cx{};
+  cx.send = plan->d_send;
+  cx.recv = plan->d_recv;
+  cx.slots = plan->d_slots;
+  cx.rootacc = plan->d_rootacc;
+  cx.entries = plan->d_entries;
+  cx.steps = plan->d_steps[vi];
+  cx.count = (int64_t)count;
+  cx.slot_chunk_stride = plan->slot_chunk_stride;
+  cx.slot_rank_stride = plan->slot_rank_stride;
+  cx.rootacc_stride = plan->rootacc_stride;
+  cx.esize = (int64_t)es;
+  cx.N = N;
+  cx.nsteps = (int32_t)plan->steps[vi].size();
+  cx.own_copy = own_copy ? 1 : 0;
+  if (plan->clock_khz == 0) {
+    int khz = 0, cus = 0;
+    HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, device));
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device));
+    plan->clock_khz = khz > 0 ? khz : 100000;
+    plan->cus = cus;
+  }
+  cx.timeout_ticks = (int64_t)timeout_us_now() * plan->clock_khz / 1000;
+  cx.bar = plan->d_sync;
+  cx.status = plan->d_sync + 2;
+
+  const pat::Variant var = variant_for(coll, dt, vec);
+  const auto& steps = plan->steps[vi];
+  const int mode = mode_now();
+  if (mode == PAT_EXEC_PERSISTENT) {
+    if (plan->capacity[var] == 0) HIP_TRY(pat::persistent_capacity(var, &plan->capacity[var]));
+    int64_t most = 1;
+    for (const auto& st : steps) most = std::max(most, st.items);
+    int64_t cap = plan->capacity[var];
+    if (const int per_cu = blocks_per_cu_cap()) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));
+    if (const char* e = std::getenv("PAT_DEBUG"))
+      if (e[0] == '1')
+        std::fprintf(stderr, "[pat] persistent launch: capacity=%d cus=%d grid=%d steps=%d\n",
+                     plan->capacity[var], plan->cus, grid, cx.nsteps);
+    HIP_TRY(pat::launch_persistent(var, cx, grid, stream));
+  } else if (mode == PAT_EXEC_STREAM) {
+    for (size_t s = 0; s < steps.size(); ++s) HIP_TRY(pat::launch_step(var, cx, (int)s, steps[s].items, stream));
+  } else {
+    hipGraphExec_t& exec = plan->graph[vi][cx.own_copy];
+    if (!exec) {
+      hipStream_t cs = nullptr;
+      HIP_TRY(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+      hipGraph_t g = nullptr;
+      hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+      for (size_t s = 0; e == hipSuccess && s < steps.size(); ++s)
+        e = pat::launch_step(var, cx, (int)s, steps[s].items, cs);
+      const hipError_t e2 = hipStreamEndCapture(cs, &g);
+      if (e == hipSuccess) e = e2;
+      if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);
+      if (g) (void)hipGraphDestroy(g);
+      (void)hipStreamDestroy(cs);
+      if (e != hipSuccess) {
+        exec = nullptr;
+        g_last_hip.store((int)e);
+        return PAT_ERR_HIP;
+      }
+    }
+    HIP_TRY(hipGraphLaunch(exec, stream));
+  }
+  return PAT_OK;
+}
+
+pat_status_t describe(int coll, int N, size_t count, pat_dtype_t dt, pat::PlanDesc* d) {
+  if (coll != 0 && coll != 1) return PAT_ERR_INVALID_ARGUMENT;
+  if (N < 1 || N > kMaxRanks) return PAT_ERR_INVALID_ARGUMENT;
+  if (dt != PAT_INT32 && dt != PAT_FLOAT32 && dt != PAT_BFLOAT16) return PAT_ERR_UNSUPPORTED;
+  if (count > (size_t(1) << 40)) return PAT_ERR_INVALID_ARGUMENT;
+  size_t budget;
+  {
+    std::lock_guard<std::mutex> lock(g_mu);
+    budget = budget_now();
+  }
+  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, d)) return PAT_ERR_INVALID_ARGUMENT;
+  return PAT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pat_status_t pat_allgather(const void* const* sendbufs, void* const* recvbufs, size_t count, pat_dtype_t dtype,
+                           int nranks, hipStream_t stream) {
+  return run(0, sendbufs, recvbufs, count, dtype, nranks, stream);
+}
+
+pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbufs, size_t count,
+                               pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream) {
+  if (op != PAT_SUM) return PAT_ERR_UNSUPPORTED;
+  return run(1, sendbufs, recvbufs, count, dtype, nranks, stream);
+}
+
+pat_status_t pat_set_buffer_bytes(size_t bytes_per_slot) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_budget = bytes_per_slot;
+  return PAT_OK;
+}
+
+size_t pat_get_buffer_bytes(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  return budget_now();
+}
+
+pat_status_t pat_set_exec_mode(int mode) {
+  if (mode < PAT_EXEC_PERSISTENT || mode > PAT_EXEC_STREAM) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_mode = mode;
+  return PAT_OK;
+}
+
+int pat_get_exec_mode(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  return mode_now();
+}
+
+pat_status_t pat_set_barrier_timeout_us(uint32_t microseconds) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_timeout_us = microseconds;
+  return PAT_OK;
+}
+
+pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,
+                           pat_plan_info_t* out) {
+  if (!out) return PAT_ERR_INVALID_ARGUMENT;
+  pat::PlanDesc d;
+  const pat_status_t s = describe((int)coll, nranks, count, dtype, &d);
+  if (s != PAT_OK) return s;
+  pat_plan_info_t info{};
+  info.nranks = nranks;
+  info.L = d.sched.L;
+  info.t = d.sched.t;
+  info.T = d.sched.T;
+  info.steps = (int)d.exec.size();
+  info.pieces = d.pieces;
+  info.max_chunks_per_step = d.max_k;
+  info.vector_path = (d.count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
+  info.count = count;
+  info.piece_elems = (size_t)d.piece_elems;
+  info.slot_elem_bytes = (size_t)d.esize_slot;
+  info.slot_dims = d.slots.dims;
+  info.slot_chunks_per_rank = d.slots.entries;
+  const size_t chunk_stride = round_up(size_t(d.piece_elems) * d.esize_slot, 256);
+  info.slot_bytes_per_rank = chunk_stride * d.slots.entries;
+  const size_t root = (coll == PAT_REDUCESCATTER && dtype == PAT_BFLOAT16) ? round_up(size_t(d.piece_elems) * 4, 256) : 0;
+  info.slot_bytes_total = (info.slot_bytes_per_rank + root) * size_t(nranks);
+  info.alg_bytes = d.alg_bytes;
+  info.bus_bytes_per_rank = double(nranks - 1) * double(count) * d.esize_in;
+  *out = info;
+  return PAT_OK;
+}
+
+pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype, int32_t* step_d,
+                            int32_t* step_k, int max_steps, int32_t* pos, int32_t* a, int32_t* b, int32_t* c,
+                            int max_entries, int* nsteps, int* nentries) {
+  if (!nsteps || !nentries) return PAT_ERR_INVALID_ARGUMENT;
+  pat::PlanDesc d;
+  const pat_status_t s = describe((int)coll, nranks, count, dtype, &d);
+  if (s != PAT_OK) return s;
+  *nsteps = (int)d.exec.size();
+  *nentries = (int)d.entries.size();
+  if (*nsteps > max_steps || *nentries > max_entries) return PAT_ERR_INVALID_ARGUMENT;
+  for (size_t i = 0; i < d.exec.size(); ++i) {
+    if (step_d) step_d[i] = d.exec[i].d;
+    if (step_k) step_k[i] = d.exec[i].k;
+  }
+  for (size_t j = 0; j < d.entries.size(); ++j) {
+    if (pos) pos[j] = d.entries[j].p;
+    if (a) a[j] = d.entries[j].a;
+    if (b) b[j] = d.entries[j].b;
+    if (c) c[j] = d.entries[j].c;
+  }
+  return PAT_OK;
+}
+
+pat_status_t pat_check_device_status(hipStream_t stream) {
+  HIP_TRY(hipStreamSynchronize(stream));
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  pat_status_t result = PAT_OK;
+  for (auto& kv : g_plans) {
+    Plan* p = kv.second.get();
+    if (p->device != device) continue;
+    unsigned h[4] = {0, 0, 0, 0};
+    HIP_TRY(hipMemcpy(h, p->d_sync, sizeof(h), hipMemcpyDeviceToHost));
+    if (h[2]) {
+      result = PAT_ERR_TIMEOUT;
+      HIP_TRY(hipMemset(p->d_sync, 0, sizeof(h)));
+    }
+  }
+  return result;
+}
+
+int pat_last_hip_error(void) { return g_last_hip.load(); }
+
+const char* pat_status_string(pat_status_t status) {
+  switch (status) {
+    case PAT_OK: return "PAT_OK";
+    case PAT_ERR_INVALID_ARGUMENT: return "PAT_ERR_INVALID_ARGUMENT";
+    case PAT_ERR_UNSUPPORTED: return "PAT_ERR_UNSUPPORTED";
+    case PAT_ERR_OUT_OF_MEMORY: return "PAT_ERR_OUT_OF_MEMORY";
+    case PAT_ERR_HIP: return "PAT_ERR_HIP";
+    case PAT_ERR_TIMEOUT: return "PAT_ERR_TIMEOUT";
+    case PAT_ERR_INTERNAL: return "PAT_ERR_INTERNAL";
+    default: return "PAT_ERR_UNKNOWN";
+  }
+}
+
+pat_status_t pat_finalize(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (g_plans.empty()) return PAT_OK;
+  int cur = 0;
+  HIP_TRY(hipGetDevice(&cur));
+  std::vector<int> devices;
+  for (auto& kv : g_plans) devices.push_back(kv.second->device);
+  std::sort(devices.begin(), devices.end());
+  devices.erase(std::unique(devices.begin(), devices.end()), devices.end());
+  for (int dev : devices) {
+    HIP_TRY(hipSetDevice(dev));
+    HIP_TRY(hipDeviceSynchronize());
+  }
+  HIP_TRY(hipSetDevice(cur));
+  g_plans.clear();
+  return PAT_OK;
+}
+
+}  // extern "C"

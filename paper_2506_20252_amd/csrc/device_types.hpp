@@ -1,0 +1,36 @@
+// Tables the host uploads and the step kernels read.  Plain structs, no HIP.
+#pragma once
+
+#include <cstdint>
+
+namespace pat {
+
+// Markers in DevEntry slot fields.
+enum : int32_t {
+  kUser = -1,       // the rank's own send buffer (raw input)
+  kRoot = -2,       // the rank's own chunk: receive buffer (int32/fp32) or float32 root accumulator (bf16)
+  kRootFinal = -3,  // the root's last receive: write the receive buffer (bf16: rounded)
+};
+
+// One chunk-edge of a step, relative to the acting rank r (16 bytes).
+//   all-gather:     p = sender position;   a = source slot | kUser;   b = receiver slot | kUser (none)
+//   reduce-scatter: p = receiver position; a = child slot | kUser (child's input);
+//                   b = own accumulator slot | kUser (own input) | kRoot;
+//                   c = destination slot | kRoot | kRootFinal
+struct DevEntry {
+  int32_t p, a, b, c;
+};
+
+// One launch-level step (a schedule step of one piece), as the kernels see it.
+struct DevStep {
+  int32_t d;               // distance: peer = r + d (all-gather) / child = r + d (reduce-scatter)
+  int32_t k;               // entries per rank
+  int32_t entry0;          // first entry in the entry table
+  int32_t first;           // 1: first step of a piece (all-gather fuses the own-chunk copy here)
+  int64_t e0;              // first element of the piece within a chunk
+  int64_t V;               // vectors per chunk-piece
+  int64_t tiles_per_edge;  // > 0: each work item is one tile of one edge; 0: items pack edges
+  int64_t items;           // work items (workgroups) of this step
+};
+
+}  // namespace pat

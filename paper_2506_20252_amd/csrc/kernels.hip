@@ -1,0 +1,519 @@
+// PAT step kernels for gfx950 (CDNA4).
+//
+// One step of the schedule is N * k independent chunk-edges (k entries of the
+// step table, for every acting rank r).  A workgroup processes one work item:
+//   tiled:  one tile of kThreads * kUnroll vectors of one edge, the edge's
+//           addresses computed once per workgroup (wavefront-uniform);
+//   packed: chunks smaller than a tile; consecutive vectors of consecutive
+//           edges, addresses computed per lane.
+// Every lane issues all of its loads before any store (kUnroll vectors of
+// 16 bytes in flight per stream).  The data path has no matrix work and no
+// reuse, so there is no LDS staging: a 128-bit load lands in VGPRs and is
+// stored from there.
+//
+// All-gather step (section "The PAT algorithm"): the sender at tree position
+// p copies chunk (r - p) mod N from its send buffer (p = 0) or from the slot
+// it arrived in, to the receiver r + d: into its receive buffer, and into its
+// slot when the receiver forwards the chunk later.  The first step also
+// copies each rank's own chunk into its receive buffer (a local copy).
+//
+// Reduce-scatter step (section "Conversion to reduce-scatter operations"):
+// the receiver at position p of tree c = (r - p) mod N loads the partial of
+// the child at p + d (its raw input if it is a leaf, else its accumulator
+// slot) and its own value (raw input at the first receive, else its
+// accumulator), adds, and stores the accumulator -- or, at the root, the
+// receive buffer.  int32 adds wrap; float32 adds round to nearest even;
+// bf16 data is widened exactly to float32 and rounded once, at the root's
+// last receive.
+//
+// Step order: steps depend on each other (a slot written at step s is read
+// at step s + 1).  Per-step launches get the ordering from the kernel
+// boundary; the persistent kernel uses a device-wide barrier whose fences
+// make every block's writes visible across the XCDs' separate L2 caches.
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace pat {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ T ldg(const char* p) {
+  return *reinterpret_cast<const T*>(p);
+}
+
+template <typename T>
+__device__ __forceinline__ void stg(char* p, const T& v) {
+  *reinterpret_cast<T*>(p) = v;
+}
+
+__device__ __forceinline__ int wrap_add(int a, int b, int n) {
+  const int s = a + b;
+  return s >= n ? s - n : s;
+}
+
+__device__ __forceinline__ int wrap_sub(int a, int b, int n) {
+  const int s = a - b;
+  return s < 0 ? s + n : s;
+}
+
+// Split a flat vector index of a packed step into (rank, entry, vector).
+__device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r, int* i, int64_t* v,
+                                           bool small) {
+  if (small) {
+    const uint32_t gg = (uint32_t)g, V = (uint32_t)st.V, k = (uint32_t)st.k;
+    const uint32_t e = gg / V;
+    *v = gg - e * V;
+    *r = (int)(e / k);
+    *i = (int)(e - (uint32_t)(*r) * k);
+  } else {
+    const int64_t e = g / st.V;
+    *v = g - e * st.V;
+    *r = (int)(e / st.k);
+    *i = (int)(e - (int64_t)(*r) * st.k);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// All-gather
+// ---------------------------------------------------------------------------
+
+template <typename Unit, int U>
+struct AgOp {
+  static constexpr int kTile = kThreads * U;
+
+  struct Edge {
+    const char* src;
+    char* dst;   // receiver's receive buffer
+    char* dst2;  // receiver's slot (null: the receiver does not forward)
+    char* dst3;  // own chunk into the sender's receive buffer (first step only)
+  };
+
+  __device__ static Edge edge(const KCtx& cx, const DevStep& st, int r, int i) {
+    const DevEntry en = cx.entries[st.entry0 + i];
+    const int c = wrap_sub(r, en.p, cx.N);
+    const int peer = wrap_add(r, st.d, cx.N);
+    const int64_t piece = st.e0 * cx.esize;
+    const int64_t chunk = cx.count * cx.esize;
+    Edge e;
+    e.src = en.a == kUser ? (const char*)cx.send[r] + piece
+                          : cx.slots + r * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.dst = (char*)cx.recv[peer] + c * chunk + piece;
+    e.dst2 = en.b >= 0 ? cx.slots + peer * cx.slot_rank_stride + en.b * cx.slot_chunk_stride : nullptr;
+    e.dst3 = (st.first && en.p == 0 && cx.own_copy) ? (char*)cx.recv[r] + r * chunk + piece : nullptr;
+    return e;
+  }
+
+  __device__ static void put(const Edge& e, int64_t v, const Unit& x) {
+    const int64_t o = v * (int64_t)sizeof(Unit);
+    stg(e.dst + o, x);
+    if (e.dst2) stg(e.dst2 + o, x);
+    if (e.dst3) stg(e.dst3 + o, x);
+  }
+
+  __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
+    Unit x[U];
+    if (st.tiles_per_edge > 0) {
+      const int64_t eid = item / st.tiles_per_edge;
+      const int64_t tile = item - eid * st.tiles_per_edge;
+      const int r = (int)(eid / st.k);
+      const int i = (int)(eid - (int64_t)r * st.k);
+      const Edge e = edge(cx, st, r, i);
+      const int64_t v0 = tile * kTile + threadIdx.x;
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t v = v0 + j * kThreads;
+        if (v < st.V) x[j] = ldg<Unit>(e.src + v * (int64_t)sizeof(Unit));
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t v = v0 + j * kThreads;
+        if (v < st.V) put(e, v, x[j]);
+      }
+    } else {
+      const int64_t units = (int64_t)cx.N * st.k * st.V;
+      const bool small = units < (int64_t(1) << 31);
+      Edge e[U];
+      int64_t vv[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t g = item * kTile + j * kThreads + threadIdx.x;
+        vv[j] = -1;
+        if (g < units) {
+          int r, i;
+          split_flat(g, st, &r, &i, &vv[j], small);
+          e[j] = edge(cx, st, r, i);
+          x[j] = ldg<Unit>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) put(e[j], vv[j], x[j]);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Reduce-scatter
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// float32 -> bf16, round to nearest, ties to even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+struct F8 {
+  float4 lo, hi;
+};
+
+struct TI32V {
+  using in_t = uint4;
+  using acc_t = uint4;
+  static constexpr int kInElem = 4;
+  static constexpr bool kSeparateRoot = false;
+  static constexpr int kUnroll = 4;
+  __device__ static acc_t widen(const in_t& x) { return x; }
+  __device__ static in_t narrow(const acc_t& x) { return x; }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
+    return make_uint4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+  }
+};
+
+struct TF32V {
+  using in_t = float4;
+  using acc_t = float4;
+  static constexpr int kInElem = 4;
+  static constexpr bool kSeparateRoot = false;
+  static constexpr int kUnroll = 4;
+  __device__ static acc_t widen(const in_t& x) { return x; }
+  __device__ static in_t narrow(const acc_t& x) { return x; }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+  }
+};
+
+struct TB16V {
+  using in_t = uint4;  // 8 bf16, element 2j in the low half of word j
+  using acc_t = F8;
+  static constexpr int kInElem = 2;
+  static constexpr bool kSeparateRoot = true;
+  static constexpr int kUnroll = 2;
+  __device__ static acc_t widen(const in_t& x) {
+    F8 r;
+    r.lo = make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y));
+    r.hi = make_float4(bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w));
+    return r;
+  }
+  __device__ static in_t narrow(const acc_t& a) {
+    return make_uint4(bf16_rne(a.lo.x) | (bf16_rne(a.lo.y) << 16), bf16_rne(a.lo.z) | (bf16_rne(a.lo.w) << 16),
+                      bf16_rne(a.hi.x) | (bf16_rne(a.hi.y) << 16), bf16_rne(a.hi.z) | (bf16_rne(a.hi.w) << 16));
+  }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
+    F8 r;
+    r.lo = make_float4(a.lo.x + b.lo.x, a.lo.y + b.lo.y, a.lo.z + b.lo.z, a.lo.w + b.lo.w);
+    r.hi = make_float4(a.hi.x + b.hi.x, a.hi.y + b.hi.y, a.hi.z + b.hi.z, a.hi.w + b.hi.w);
+    return r;
+  }
+};
+
+struct TI32S {
+  using in_t = uint32_t;
+  using acc_t = uint32_t;
+  static constexpr int kInElem = 4;
+  static constexpr bool kSeparateRoot = false;
+  static constexpr int kUnroll = 4;
+  __device__ static acc_t widen(in_t x) { return x; }
+  __device__ static in_t narrow(acc_t x) { return x; }
+  __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
+};
+
+struct TF32S {
+  using in_t = float;
+  using acc_t = float;
+  static constexpr int kInElem = 4;
+  static constexpr bool kSeparateRoot = false;
+  static constexpr int kUnroll = 4;
+  __device__ static acc_t widen(in_t x) { return x; }
+  __device__ static in_t narrow(acc_t x) { return x; }
+  __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
+};
+
+struct TB16S {
+  using in_t = uint16_t;
+  using acc_t = float;
+  static constexpr int kInElem = 2;
+  static constexpr bool kSeparateRoot = true;
+  static constexpr int kUnroll = 4;
+  __device__ static acc_t widen(in_t x) { return __uint_as_float((uint32_t)x << 16); }
+  __device__ static in_t narrow(acc_t x) { return (uint16_t)bf16_rne(x); }
+  __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
+};
+
+template <class R>
+struct RsOp {
+  using in_t = typename R::in_t;
+  using acc_t = typename R::acc_t;
+  static constexpr int U = R::kUnroll;
+  static constexpr int kTile = kThreads * U;
+
+  struct Edge {
+    const char* child;
+    const char* own;
+    char* dst;
+    bool child_in;   // child is a leaf: its raw input
+    bool own_in;     // first receive: the own raw input
+    bool dst_final;  // root's last receive (bf16): store rounded to the receive buffer
+  };
+
+  __device__ static char* root(const KCtx& cx, const DevStep& st, int r) {
+    if (R::kSeparateRoot) return cx.rootacc + r * cx.rootacc_stride;
+    return (char*)cx.recv[r] + st.e0 * R::kInElem;
+  }
+
+  __device__ static Edge edge(const KCtx& cx, const DevStep& st, int r, int i) {
+    const DevEntry en = cx.entries[st.entry0 + i];
+    const int c = wrap_sub(r, en.p, cx.N);
+    const int child = wrap_add(r, st.d, cx.N);
+    const int64_t uoff = (c * cx.count + st.e0) * R::kInElem;
+    Edge e;
+    e.child_in = en.a == kUser;
+    e.child = e.child_in ? (const char*)cx.send[child] + uoff
+                         : cx.slots + child * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.own_in = en.b == kUser;
+    e.own = e.own_in ? (const char*)cx.send[r] + uoff
+            : en.b == kRoot ? root(cx, st, r)
+                            : cx.slots + r * cx.slot_rank_stride + en.b * cx.slot_chunk_stride;
+    e.dst_final = R::kSeparateRoot && en.c == kRootFinal;
+    e.dst = en.c >= 0 ? cx.slots + r * cx.slot_rank_stride + en.c * cx.slot_chunk_stride
+            : e.dst_final ? (char*)cx.recv[r] + st.e0 * R::kInElem
+                          : root(cx, st, r);
+    return e;
+  }
+
+  __device__ static acc_t load(const char* p, bool raw, int64_t v) {
+    if (raw) return R::widen(ldg<in_t>(p + v * (int64_t)sizeof(in_t)));
+    return ldg<acc_t>(p + v * (int64_t)sizeof(acc_t));
+  }
+
+  __device__ static void store(const Edge& e, int64_t v, const acc_t& x) {
+    if (e.dst_final)
+      stg(e.dst + v * (int64_t)sizeof(in_t), R::narrow(x));
+    else
+      stg(e.dst + v * (int64_t)sizeof(acc_t), x);
+  }
+
+  __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
+    acc_t a[U], b[U];
+    if (st.tiles_per_edge > 0) {
+      const int64_t eid = item / st.tiles_per_edge;
+      const int64_t tile = item - eid * st.tiles_per_edge;
+      const int r = (int)(eid / st.k);
+      const int i = (int)(eid - (int64_t)r * st.k);
+      const Edge e = edge(cx, st, r, i);
+      const int64_t v0 = tile * kTile + threadIdx.x;
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t v = v0 + j * kThreads;
+        if (v < st.V) {
+          a[j] = load(e.own, e.own_in, v);
+          b[j] = load(e.child, e.child_in, v);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t v = v0 + j * kThreads;
+        if (v < st.V) store(e, v, R::add(a[j], b[j]));
+      }
+    } else {
+      const int64_t units = (int64_t)cx.N * st.k * st.V;
+      const bool small = units < (int64_t(1) << 31);
+      Edge e[U];
+      int64_t vv[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t g = item * kTile + j * kThreads + threadIdx.x;
+        vv[j] = -1;
+        if (g < units) {
+          int r, i;
+          split_flat(g, st, &r, &i, &vv[j], small);
+          e[j] = edge(cx, st, r, i);
+          a[j] = load(e[j].own, e[j].own_in, vv[j]);
+          b[j] = load(e[j].child, e[j].child_in, vv[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) store(e[j], vv[j], R::add(a[j], b[j]));
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Drivers
+// ---------------------------------------------------------------------------
+
+template <class Op>
+__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, int s) {
+  const DevStep st = cx.steps[s];
+  for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
+}
+
+// Device-wide barrier for the persistent kernel.  Every thread fences its
+// writes at agent scope (write-back of this XCD's L2), one thread per block
+// counts in and polls until every block has arrived or the wall-clock limit
+// passes, and every thread fences again before reading what other blocks
+// wrote.  Returns false if the wait gave up (status bit set); the block then
+// stops.
+__device__ bool grid_barrier(const KCtx& cx, unsigned target, int* s_ok) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(&cx.bar[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const long long t0 = wall_clock64();
+    int ok = 1;
+    while ((int)(__hip_atomic_load(&cx.bar[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+      __builtin_amdgcn_s_sleep(2);
+      if (wall_clock64() - t0 > cx.timeout_ticks) {
+        __hip_atomic_fetch_or(cx.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+    }
+    *s_ok = ok;
+  }
+  __syncthreads();
+  __threadfence();
+  return *s_ok != 0;
+}
+
+template <class Op>
+__global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
+  __shared__ int s_ok;
+  unsigned target = 0;
+  bool ok = true;
+  for (int s = 0; s < cx.nsteps && ok; ++s) {
+    const DevStep st = cx.steps[s];
+    for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
+    if (s + 1 < cx.nsteps) {
+      target += gridDim.x;
+      ok = grid_barrier(cx, target, &s_ok);
+    }
+  }
+  // Leave the counters at zero for the next launch: the last block out
+  // (every block has passed every barrier by then) resets them.
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned done =
+        __hip_atomic_fetch_add(&cx.bar[1], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+    if (done == gridDim.x) {
+      __hip_atomic_store(&cx.bar[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&cx.bar[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+template <class Op>
+hipError_t launch_step_t(const KCtx& cx, int s, int64_t items, hipStream_t stream) {
+  if (items <= 0) return hipSuccess;
+  const int64_t cap = int64_t(1) << 30;
+  const unsigned grid = (unsigned)(items < cap ? items : cap);
+  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, s);
+  return hipGetLastError();
+}
+
+template <class Op>
+hipError_t launch_persistent_t(const KCtx& cx, int grid, hipStream_t stream) {
+  KCtx local = cx;
+  void* args[] = {&local};
+  return hipLaunchCooperativeKernel((const void*)persistent_kernel<Op>, dim3(grid), dim3(kThreads), args, 0,
+                                    stream);
+}
+
+template <class Op>
+hipError_t capacity_t(int* blocks) {
+  int dev = 0, per_cu = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, persistent_kernel<Op>, kThreads, 0);
+  if (e != hipSuccess) return e;
+  *blocks = per_cu * cus;
+  return hipSuccess;
+}
+
+using AgV = AgOp<uint4, 4>;
+using Ag4 = AgOp<uint32_t, 4>;
+using Ag2 = AgOp<uint16_t, 4>;
+
+#define PAT_DISPATCH(v, CALL)                    \
+  switch (v) {                                   \
+    case kAgVec: return CALL(AgV);               \
+    case kAgS4: return CALL(Ag4);                \
+    case kAgS2: return CALL(Ag2);                \
+    case kRsI32Vec: return CALL(RsOp<TI32V>);    \
+    case kRsF32Vec: return CALL(RsOp<TF32V>);    \
+    case kRsB16Vec: return CALL(RsOp<TB16V>);    \
+    case kRsI32S: return CALL(RsOp<TI32S>);      \
+    case kRsF32S: return CALL(RsOp<TF32S>);      \
+    case kRsB16S: return CALL(RsOp<TB16S>);      \
+    default: return hipErrorInvalidValue;        \
+  }
+
+}  // namespace
+
+int variant_in_bytes(Variant v) {
+  switch (v) {
+    case kAgVec:
+    case kRsI32Vec:
+    case kRsF32Vec:
+    case kRsB16Vec: return 16;
+    case kAgS4:
+    case kRsI32S:
+    case kRsF32S: return 4;
+    case kAgS2:
+    case kRsB16S: return 2;
+    default: return 0;
+  }
+}
+
+int variant_tile(Variant v) {
+  switch (v) {
+    case kAgVec: return AgV::kTile;
+    case kAgS4: return Ag4::kTile;
+    case kAgS2: return Ag2::kTile;
+    case kRsI32Vec: return RsOp<TI32V>::kTile;
+    case kRsF32Vec: return RsOp<TF32V>::kTile;
+    case kRsB16Vec: return RsOp<TB16V>::kTile;
+    case kRsI32S: return RsOp<TI32S>::kTile;
+    case kRsF32S: return RsOp<TF32S>::kTile;
+    case kRsB16S: return RsOp<TB16S>::kTile;
+    default: return 0;
+  }
+}
+
+hipError_t launch_step(Variant v, const KCtx& cx, int s, int64_t items, hipStream_t stream) {
+#define PAT_STEP(OP) launch_step_t<OP>(cx, s, items, stream)
+  PAT_DISPATCH(v, PAT_STEP)
+#undef PAT_STEP
+}
+
+hipError_t launch_persistent(Variant v, const KCtx& cx, int grid, hipStream_t stream) {
+#define PAT_PERS(OP) launch_persistent_t<OP>(cx, grid, stream)
+  PAT_DISPATCH(v, PAT_PERS)
+#undef PAT_PERS
+}
+
+hipError_t persistent_capacity(Variant v, int* blocks) {
+#define PAT_CAP(OP) capacity_t<OP>(blocks)
+  PAT_DISPATCH(v, PAT_CAP)
+#undef PAT_CAP
+}
+
+}  // namespace pat

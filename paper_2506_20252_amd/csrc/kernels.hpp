@@ -1,0 +1,58 @@
+// Step kernels: host-side launch interface.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+#include "device_types.hpp"
+
+namespace pat {
+
+constexpr int kThreads = 256;  // workgroup size: 4 wavefronts of 64
+
+// Everything a step kernel needs, passed by value (device pointers only).
+struct KCtx {
+  const void* const* send;    // [N] device pointers (library-owned device table)
+  void* const* recv;          // [N]
+  char* slots;                // slot area: rank r's entries start at r * slot_rank_stride
+  char* rootacc;              // bf16 reduce-scatter: float32 root accumulators, [N][piece]
+  const DevEntry* entries;
+  const DevStep* steps;
+  int64_t count;              // elements per chunk
+  int64_t slot_chunk_stride;  // bytes per slot entry
+  int64_t slot_rank_stride;   // bytes per rank's slot area
+  int64_t rootacc_stride;     // bytes per rank's root accumulator
+  int64_t esize;              // bytes per user element
+  int32_t N;
+  int32_t nsteps;             // launch-level steps (schedule steps x pieces)
+  int32_t own_copy;           // all-gather: copy the own chunk (0 when in place)
+  uint32_t pad0;
+  int64_t timeout_ticks;      // persistent barrier: wall-clock ticks to wait before giving up
+  unsigned* bar;              // [2] persistent barrier: arrivals, exits (zero between launches)
+  unsigned* status;           // [1] bit 0: a barrier timed out
+};
+
+enum Variant : int {
+  kAgVec = 0,   // all-gather, 16-byte units
+  kAgS4,        // all-gather, 4-byte elements
+  kAgS2,        // all-gather, 2-byte elements
+  kRsI32Vec,
+  kRsF32Vec,
+  kRsB16Vec,    // bf16 in, float32 partials
+  kRsI32S,
+  kRsF32S,
+  kRsB16S,
+  kNumVariants
+};
+
+// Bytes of user data per vector, and vectors per work-item tile.
+int variant_in_bytes(Variant v);
+int variant_tile(Variant v);
+
+hipError_t launch_step(Variant v, const KCtx& cx, int s, int64_t items, hipStream_t stream);
+hipError_t launch_persistent(Variant v, const KCtx& cx, int grid, hipStream_t stream);
+// Workgroups of the persistent kernel that fit on the current device at once.
+hipError_t persistent_capacity(Variant v, int* blocks);
+
+}  // namespace pat

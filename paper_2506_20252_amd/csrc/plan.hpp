@@ -1,0 +1,88 @@
+// Host-side PAT plan: schedule generation, slot layout and the byte model.
+//
+// Pure C++ (no HIP): the library builds every table here once per
+// (collective, ranks, count, dtype, budget) and uploads it; the device never
+// computes the schedule.  The paper notes that computing the steps is itself
+// linear work (section "Performance"), so it is hoisted out of the hot path.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "device_types.hpp"
+
+namespace pat {
+
+int ceil_log2(int64_t n);
+
+// One step of the relative all-gather schedule: every rank r sends, for each
+// tree position p in pos[first .. first + k), chunk (r - p) mod N to rank
+// (r + d) mod N.  The table is the same for every rank up to the shift r.
+struct StepSpec {
+  int32_t d;
+  int32_t k;
+  int32_t first;
+};
+
+struct Schedule {
+  int N = 0, L = 0, t = 0, T = 1, M = 1;
+  std::vector<StepSpec> steps;  // all-gather order
+  std::vector<int32_t> pos;     // sender positions, step after step
+};
+
+// Steps for N ranks and T = 2^t parallel sub-trees (section "The PAT
+// algorithm"): the top t distances fully aggregated, farthest first; then a
+// far-first pre-order walk of a span-M sub-tree (M = 2^(L - t)), every walk
+// edge taken in all T sub-trees at once.  Edges a truncated tree lacks are
+// dropped, and so is a step left empty.
+Schedule make_schedule(int N, int t);
+
+int max_chunks_per_step(const Schedule& s);
+
+// Intermediate-buffer layout of one rank.  A node of a tree that forwards
+// (all-gather) or accumulates (reduce-scatter) keeps the chunk in the slot of
+// the distance D it arrived on / will leave on, D = lowest set bit of its
+// position p, at index p / max(2D, M): the top distances use each slot once,
+// and a linear-part slot holds one chunk per sub-tree because the far-first
+// walk drains it before the same distance is used again.
+struct SlotMap {
+  int N = 0, L = 0, M = 1;
+  std::vector<int32_t> base;  // by log2 D: first entry of that distance's slot
+  std::vector<int32_t> cap;   // by log2 D: entries of that slot
+  int32_t entries = 0;        // chunk-sized entries per rank
+  int dims = 0;               // distances that need a slot
+  // Entry index of position p, or -1 if that node neither forwards nor accumulates.
+  int32_t index(int p) const;
+};
+
+SlotMap make_slot_map(int N, int L, int M);
+
+struct PlanDesc {
+  int coll = 0;        // 0 all-gather, 1 reduce-scatter
+  int N = 0;
+  int dtype = 0;
+  int64_t count = 0;
+  int esize_in = 0;    // bytes per user element
+  int esize_slot = 0;  // bytes per slot element (float32 partials for bf16 sums)
+  Schedule sched;
+  SlotMap slots;
+  std::vector<DevEntry> entries;   // execution order
+  std::vector<StepSpec> exec;      // execution order (reduce-scatter: reversed)
+  int pieces = 1;
+  int64_t piece_elems = 0;
+  int max_k = 0;
+  double alg_bytes = 0.0;
+};
+
+// Budget in bytes per slot.  Returns false for unsupported arguments.
+bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, PlanDesc* out);
+
+// Algorithmic memory bytes of one operation (read + written by the steps):
+// all-gather: per chunk-edge, read C, write C to the receiver's buffer, write
+// C again to its slot when it forwards (plus each rank's own chunk, C);
+// reduce-scatter: per chunk-edge, read the child's partial, read the
+// receiver's own input or accumulator, write the accumulator.
+double algorithmic_bytes(const PlanDesc& d);
+
+}  // namespace pat

@@ -1,0 +1,205 @@
+"""ctypes binding of libpat.so: the C-ABI declared in include/pat.h, same names.
+
+Argument marshalling only: every step of the collective runs in the HIP
+kernels of the library.  Buffers may be given as integers (device addresses)
+or as objects with ``data_ptr()`` (e.g. torch tensors); streams as integers
+(hipStream_t) or objects with ``cuda_stream`` (torch streams); None is the
+default stream.  Functions return the pat_status_t code, like the C calls;
+``check()`` turns a non-zero code into an exception.
+
+If the library is not built, loading it raises: there is no fallback.
+"""
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpat.so")
+
+PAT_OK = 0
+PAT_ERR_INVALID_ARGUMENT = 1
+PAT_ERR_UNSUPPORTED = 2
+PAT_ERR_OUT_OF_MEMORY = 3
+PAT_ERR_HIP = 4
+PAT_ERR_TIMEOUT = 5
+PAT_ERR_INTERNAL = 6
+
+PAT_INT32 = 0
+PAT_FLOAT32 = 1
+PAT_BFLOAT16 = 2
+DTYPES = {"int32": PAT_INT32, "float32": PAT_FLOAT32, "bfloat16": PAT_BFLOAT16}
+ELEM_BYTES = {PAT_INT32: 4, PAT_FLOAT32: 4, PAT_BFLOAT16: 2}
+
+PAT_SUM = 0
+
+PAT_ALLGATHER = 0
+PAT_REDUCESCATTER = 1
+
+PAT_EXEC_PERSISTENT = 0
+PAT_EXEC_GRAPH = 1
+PAT_EXEC_STREAM = 2
+MODES = {"persistent": PAT_EXEC_PERSISTENT, "graph": PAT_EXEC_GRAPH, "stream": PAT_EXEC_STREAM}
+
+# Every function include/pat.h declares.
+EXPORTS = (
+    "pat_allgather", "pat_reducescatter", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
+    "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_barrier_timeout_us", "pat_plan_info",
+    "pat_plan_steps", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
+    "pat_finalize",
+)
+
+
+class pat_plan_info_t(ctypes.Structure):
+    _fields_ = [
+        ("nranks", ctypes.c_int), ("L", ctypes.c_int), ("t", ctypes.c_int), ("T", ctypes.c_int),
+        ("steps", ctypes.c_int), ("pieces", ctypes.c_int), ("max_chunks_per_step", ctypes.c_int),
+        ("vector_path", ctypes.c_int), ("count", ctypes.c_size_t), ("piece_elems", ctypes.c_size_t),
+        ("slot_elem_bytes", ctypes.c_size_t), ("slot_dims", ctypes.c_int),
+        ("slot_chunks_per_rank", ctypes.c_int), ("slot_bytes_per_rank", ctypes.c_size_t),
+        ("slot_bytes_total", ctypes.c_size_t), ("alg_bytes", ctypes.c_double),
+        ("bus_bytes_per_rank", ctypes.c_double),
+    ]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class PatError(RuntimeError):
+    def __init__(self, status, where=""):
+        self.status = status
+        super().__init__(f"{where}: {pat_status_string(status)}"
+                         + (f" (hipError {pat_last_hip_error()})" if status == PAT_ERR_HIP else ""))
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32P = ctypes.POINTER(ctypes.c_int32)
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        sig = {
+            "pat_allgather": ([_P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _P], ctypes.c_int),
+            "pat_reducescatter": ([_P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P],
+                                  ctypes.c_int),
+            "pat_set_buffer_bytes": ([ctypes.c_size_t], ctypes.c_int),
+            "pat_get_buffer_bytes": ([], ctypes.c_size_t),
+            "pat_set_exec_mode": ([ctypes.c_int], ctypes.c_int),
+            "pat_get_exec_mode": ([], ctypes.c_int),
+            "pat_set_barrier_timeout_us": ([ctypes.c_uint32], ctypes.c_int),
+            "pat_plan_info": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
+                               ctypes.POINTER(pat_plan_info_t)], ctypes.c_int),
+            "pat_plan_steps": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, _I32P, _I32P,
+                                ctypes.c_int, _I32P, _I32P, _I32P, _I32P, ctypes.c_int,
+                                ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
+            "pat_check_device_status": ([_P], ctypes.c_int),
+            "pat_last_hip_error": ([], ctypes.c_int),
+            "pat_status_string": ([ctypes.c_int], ctypes.c_char_p),
+            "pat_finalize": ([], ctypes.c_int),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def check(status, where="pat"):
+    if status != PAT_OK:
+        raise PatError(status, where)
+    return status
+
+
+def _dtype(dtype):
+    return DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+
+
+def _addr(b):
+    return int(b.data_ptr()) if hasattr(b, "data_ptr") else int(b)
+
+
+def _ptr_array(bufs):
+    vals = [_addr(b) for b in bufs]
+    return (ctypes.c_void_p * max(len(vals), 1))(*vals)
+
+
+def _stream(stream):
+    if stream is None:
+        return None
+    if hasattr(stream, "cuda_stream"):
+        return int(stream.cuda_stream)
+    return int(stream)
+
+
+def pat_allgather(sendbufs, recvbufs, count, dtype, nranks, stream=None):
+    return lib().pat_allgather(_ptr_array(sendbufs), _ptr_array(recvbufs), int(count), _dtype(dtype),
+                               int(nranks), _stream(stream))
+
+
+def pat_reducescatter(sendbufs, recvbufs, count, dtype, op, nranks, stream=None):
+    return lib().pat_reducescatter(_ptr_array(sendbufs), _ptr_array(recvbufs), int(count), _dtype(dtype),
+                                   int(op), int(nranks), _stream(stream))
+
+
+def pat_set_buffer_bytes(nbytes):
+    return lib().pat_set_buffer_bytes(int(nbytes))
+
+
+def pat_get_buffer_bytes():
+    return int(lib().pat_get_buffer_bytes())
+
+
+def pat_set_exec_mode(mode):
+    return lib().pat_set_exec_mode(MODES[mode] if isinstance(mode, str) else int(mode))
+
+
+def pat_get_exec_mode():
+    return int(lib().pat_get_exec_mode())
+
+
+def pat_set_barrier_timeout_us(microseconds):
+    return lib().pat_set_barrier_timeout_us(int(microseconds))
+
+
+def pat_plan_info(coll, nranks, count, dtype):
+    """Returns (status, dict)."""
+    info = pat_plan_info_t()
+    st = lib().pat_plan_info(int(coll), int(nranks), int(count), _dtype(dtype), ctypes.byref(info))
+    return st, info.as_dict()
+
+
+def pat_plan_steps(coll, nranks, count, dtype):
+    """Returns (status, steps, entries): steps = [(d, k)], entries = [(p, a, b, c)]."""
+    n = max(int(nranks), 1)
+    d = (ctypes.c_int32 * n)()
+    k = (ctypes.c_int32 * n)()
+    pos, a, b, c = [(ctypes.c_int32 * n)() for _ in range(4)]
+    ns, ne = ctypes.c_int(), ctypes.c_int()
+    st = lib().pat_plan_steps(int(coll), int(nranks), int(count), _dtype(dtype), d, k, n, pos, a, b, c, n,
+                              ctypes.byref(ns), ctypes.byref(ne))
+    if st != PAT_OK:
+        return st, [], []
+    steps = [(d[i], k[i]) for i in range(ns.value)]
+    entries = [(pos[j], a[j], b[j], c[j]) for j in range(ne.value)]
+    return st, steps, entries
+
+
+def pat_check_device_status(stream=None):
+    return lib().pat_check_device_status(_stream(stream))
+
+
+def pat_last_hip_error():
+    return int(lib().pat_last_hip_error())
+
+
+def pat_status_string(status):
+    return lib().pat_status_string(int(status)).decode()
+
+
+def pat_finalize():
+    return lib().pat_finalize()

@@ -1,0 +1,113 @@
+"""C-ABI boundary checks that need no GPU: the library loads, exports every
+function include/pat.h declares, and rejects bad arguments before touching
+the device."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_20252_amd import pat
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "pat.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pat_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 13
+    lib = ctypes.CDLL(pat.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(pat.EXPORTS) == names
+
+
+def test_status_strings():
+    assert pat.pat_status_string(pat.PAT_OK) == "PAT_OK"
+    assert pat.pat_status_string(pat.PAT_ERR_TIMEOUT) == "PAT_ERR_TIMEOUT"
+    assert pat.pat_status_string(99) == "PAT_ERR_UNKNOWN"
+
+
+def fake(base, n, stride):
+    return [base + i * stride for i in range(n)]
+
+
+def test_argument_errors_before_any_device_call():
+    ok_send = fake(0x100000, 4, 0x10000)
+    ok_recv = fake(0x900000, 4, 0x10000)
+    # count == 0 is a no-op
+    assert pat.pat_allgather(ok_send, ok_recv, 0, "float32", 4) == pat.PAT_OK
+    assert pat.pat_reducescatter(ok_send, ok_recv, 0, "int32", pat.PAT_SUM, 4) == pat.PAT_OK
+    # rank count
+    assert pat.pat_allgather(ok_send, ok_recv, 16, "float32", 0) == pat.PAT_ERR_INVALID_ARGUMENT
+    assert pat.pat_allgather(ok_send, ok_recv, 16, "float32", -3) == pat.PAT_ERR_INVALID_ARGUMENT
+    # dtype / op
+    assert pat.pat_allgather(ok_send, ok_recv, 16, 7, 4) == pat.PAT_ERR_UNSUPPORTED
+    assert pat.pat_reducescatter(ok_send, ok_recv, 16, "float32", 3, 4) == pat.PAT_ERR_UNSUPPORTED
+    # null buffer
+    assert pat.pat_allgather(ok_send[:3] + [0], ok_recv, 16, "float32", 4) == pat.PAT_ERR_INVALID_ARGUMENT
+    # element misalignment
+    bad = list(ok_send)
+    bad[2] += 2
+    assert pat.pat_allgather(bad, ok_recv, 16, "float32", 4) == pat.PAT_ERR_INVALID_ARGUMENT
+    # receive buffers overlapping each other (all-gather: 4 * 16 * 4 bytes each)
+    assert pat.pat_allgather(ok_send, fake(0x900000, 4, 64), 16, "float32", 4) == pat.PAT_ERR_INVALID_ARGUMENT
+    # a send buffer inside another rank's receive buffer
+    assert pat.pat_allgather([0x900000 + 64] + ok_send[1:], ok_recv, 16, "float32", 4) == \
+        pat.PAT_ERR_INVALID_ARGUMENT
+    # in place, but at the wrong chunk
+    inplace_wrong = [ok_recv[r] + ((r + 1) % 4) * 64 for r in range(4)]
+    assert pat.pat_allgather(inplace_wrong, ok_recv, 16, "float32", 4) == pat.PAT_ERR_INVALID_ARGUMENT
+    # reduce-scatter: receive buffer inside the own send buffer but not at chunk r
+    rs_wrong = [ok_send[r] + ((r + 1) % 4) * 64 for r in range(4)]
+    assert pat.pat_reducescatter(ok_send, rs_wrong, 16, "float32", pat.PAT_SUM, 4) == \
+        pat.PAT_ERR_INVALID_ARGUMENT
+
+
+def test_settings_roundtrip():
+    assert pat.pat_set_exec_mode(5) == pat.PAT_ERR_INVALID_ARGUMENT
+    old = pat.pat_get_exec_mode()
+    assert pat.pat_set_exec_mode("stream") == pat.PAT_OK and pat.pat_get_exec_mode() == pat.PAT_EXEC_STREAM
+    assert pat.pat_set_exec_mode(old) == pat.PAT_OK
+    assert pat.pat_set_buffer_bytes(1 << 20) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 1 << 20
+    assert pat.pat_set_buffer_bytes(0) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 8 << 20
+    assert pat.pat_finalize() == pat.PAT_OK  # nothing allocated: no device call
+
+
+def test_plan_info_workloads():
+    mib = 1 << 20
+    cases = [
+        # (coll, N, count, dtype, steps, T, pieces)
+        (pat.PAT_REDUCESCATTER, 6, 1024, "int32", 3, 4, 1),
+        (pat.PAT_ALLGATHER, 24, 32768, "bfloat16", 5, 16, 1),
+        (pat.PAT_REDUCESCATTER, 64, 262144, "float32", 10, 8, 1),
+        (pat.PAT_ALLGATHER, 1000, 64, "float32", 10, 512, 1),
+        (pat.PAT_REDUCESCATTER, 1000, 64, "float32", 10, 512, 1),
+        (pat.PAT_REDUCESCATTER, 128, 2 * mib, "bfloat16", 127, 1, 1),
+    ]
+    for coll, n, count, dt, steps, T, pieces in cases:
+        st, info = pat.pat_plan_info(coll, n, count, dt)
+        assert st == pat.PAT_OK
+        assert (info["steps"], info["T"], info["pieces"]) == (steps, T, pieces), (n, info)
+        assert info["slot_dims"] <= info["L"]
+    # bf16 reduce-scatter carries float32 partials
+    st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, 128, 2 * mib, "bfloat16")
+    assert info["slot_elem_bytes"] == 4
+    assert info["alg_bytes"] == pytest.approx(316.5 * 2**30, rel=1e-3)
+    # a chunk larger than the budget: T = 1, pieces
+    pat.pat_set_buffer_bytes(1 << 20)
+    try:
+        st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, 64, 262144 * 3, "float32")
+        assert info["T"] == 1 and info["pieces"] == 3 and info["steps"] == 63
+        # logarithmic buffers, independent of size: same slot entries per rank at any count
+        sizes = {pat.pat_plan_info(pat.PAT_ALLGATHER, 37, c, "float32")[1]["slot_chunks_per_rank"]
+                 for c in (1 << 18, 1 << 19, 1 << 21)}
+        assert len(sizes) == 1
+    finally:
+        pat.pat_set_buffer_bytes(0)

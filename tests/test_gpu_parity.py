@@ -1,0 +1,272 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle.
+
+Bars:
+* all-gather: bit-exact (a byte copy);
+* reduce-scatter int32: bit-exact (wrapping sum);
+* reduce-scatter float32: bit-exact against the oracle executing the PAT
+  steps (same association), and |got - sum| <= 1e-5 * sum|v| against the fp64
+  plain sum;
+* reduce-scatter bf16 (float32 partials): bit-exact against the oracle's PAT
+  order, and within 1e-2 * sum|v| of the fp64 plain sum.
+
+Inputs come from the seeded generator (device fill, host twin); the large
+workloads are checked on sampled element positions the oracle computes one by
+one (every element position is an independent reduction).
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import definitions as D
+from oracle import pat as opat
+from paper_2506_20252_amd import pat
+
+pytestmark = pytest.mark.gpu
+
+TORCH = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}
+DIST = {"int32": "int32_pm2p20", "float32": "f32_normal", "bfloat16": "bf16_normal"}
+MIB = 1 << 20
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    pat.lib()
+    torch.cuda.set_device(0)
+    os.environ["PAT_POISON_SLOTS"] = "1"  # slots start as 0xFF.. (NaN for floats)
+    pat.check(pat.pat_finalize())
+    yield
+    pat.check(pat.pat_finalize())
+    os.environ.pop("PAT_POISON_SLOTS", None)
+    torch.cuda.empty_cache()
+
+
+def as_bits(t):
+    """Device tensor -> numpy with the oracle's conventions (bf16 as uint16)."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def fill_ranks(buf, dist, seed):
+    for x in range(buf.shape[0]):
+        synth.fill(buf[x], dist, seed, x)
+
+
+def host_rs_inputs(n, count, dist, seed, sample=None):
+    """(N, N, m): rank x's contribution to chunk R at the sampled positions."""
+    if sample is None:
+        return np.stack([synth.host_buffer(dist, seed, x, n * count) for x in range(n)]).reshape(n, n, count)
+    idx = (np.arange(n, dtype=np.uint64)[:, None] * np.uint64(count) + sample.astype(np.uint64)[None, :])
+    return np.stack([synth.host_values(dist, seed, x, idx.ravel()).reshape(n, len(sample)) for x in range(n)])
+
+
+def check_rs(got, host_in, dtype, budget_t):
+    """got: (N, m) from the device; host_in: (N, N, m)."""
+    if dtype == "int32":
+        ref = D.reducescatter_sum(host_in, "int32")
+        np.testing.assert_array_equal(got, ref)
+        return
+    pat_ref, _ = opat.reducescatter(host_in, budget_t, dtype)
+    width = np.uint32 if dtype == "float32" else np.uint16
+    mism = np.count_nonzero(got.view(width) != pat_ref.view(width))
+    assert mism == 0, f"{mism} elements differ from the PAT-order oracle"
+    exact = D.reducescatter_sum(host_in, dtype)
+    scale = D.reducescatter_abs_sum(host_in, dtype)
+    val = got.astype(np.float64) if dtype == "float32" else D.bf16_bits_to_f32(got).astype(np.float64)
+    tol = 1e-5 if dtype == "float32" else 1e-2
+    assert (np.abs(val - exact) <= tol * scale).all()
+
+
+def oracle_t(coll, n, count, dtype):
+    slot = 4 if (coll == pat.PAT_REDUCESCATTER or dtype != "bfloat16") else 2
+    return opat.aggregation_level(n, count * slot, pat.pat_get_buffer_bytes())
+
+
+def run_rs(n, count, dtype, seed, mode="persistent", inplace=False, sample=None, dist=None):
+    log(f"[gpu] reduce-scatter n={n} count={count} dtype={dtype} seed={seed:#x} mode={mode} inplace={inplace}")
+    dev = torch.device("cuda:0")
+    send = torch.empty((n, n * count), dtype=TORCH[dtype], device=dev)
+    fill_ranks(send, dist or DIST[dtype], seed)
+    if inplace:
+        recvs = [send[r, r * count:(r + 1) * count] for r in range(n)]
+    else:
+        recv = torch.empty((n, count), dtype=TORCH[dtype], device=dev)
+        recv.view(torch.uint8).fill_(0x7F)
+        recvs = list(recv)
+    pat.check(pat.pat_set_exec_mode(mode))
+    stream = torch.cuda.current_stream()
+    pat.check(pat.pat_reducescatter(list(send), recvs, count, dtype, pat.PAT_SUM, n, stream), "rs")
+    pat.check(pat.pat_check_device_status(stream), "status")
+    out = torch.stack(recvs)
+    if sample is not None:
+        out = out[:, torch.as_tensor(sample, device=dev)]
+    got = as_bits(out)
+    del send, recvs, out
+    return got
+
+
+def run_ag(n, count, dtype, seed, mode="persistent", inplace=False, dist=None):
+    log(f"[gpu] all-gather n={n} count={count} dtype={dtype} seed={seed:#x} mode={mode} inplace={inplace}")
+    dist = dist or DIST[dtype]
+    dev = torch.device("cuda:0")
+    recv = torch.empty((n, n * count), dtype=TORCH[dtype], device=dev)
+    recv.view(torch.uint8).fill_(0xA5)
+    if inplace:
+        sends = [recv[r, r * count:(r + 1) * count] for r in range(n)]
+        for r in range(n):
+            synth.fill(sends[r], dist, seed, r)
+    else:
+        send = torch.empty((n, count), dtype=TORCH[dtype], device=dev)
+        fill_ranks(send, dist, seed)
+        sends = list(send)
+    pat.check(pat.pat_set_exec_mode(mode))
+    stream = torch.cuda.current_stream()
+    pat.check(pat.pat_allgather(sends, list(recv), count, dtype, n, stream), "ag")
+    pat.check(pat.pat_check_device_status(stream), "status")
+    got = as_bits(recv).reshape(n, n, count)
+    host_in = np.stack([synth.host_buffer(dist, seed, x, count) for x in range(n)])
+    return got, host_in
+
+
+# ---------------------------------------------------------------------------
+# The generator itself: device fill == host twin
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dist", ["int32_pm2p20", "f32_pm1", "f32_normal", "bf16_normal"])
+def test_device_fill_matches_host_twin(dist):
+    log(f"[gpu] synth fill {dist}")
+    dt = {"int32_pm2p20": torch.int32, "f32_pm1": torch.float32, "f32_normal": torch.float32,
+          "bf16_normal": torch.bfloat16}[dist]
+    buf = torch.empty(100003, dtype=dt, device="cuda:0")
+    synth.fill(buf, dist, 0x1234, 7)
+    want = synth.host_buffer(dist, 0x1234, 7, 100003)
+    got = as_bits(buf)
+    np.testing.assert_array_equal(got.view(want.dtype), want)
+
+
+# ---------------------------------------------------------------------------
+# The five workloads
+# ---------------------------------------------------------------------------
+
+def test_workload1_rs_int32_n6():
+    n, count, seed = 6, 1024, 0x5041541
+    got = run_rs(n, count, "int32", seed)
+    check_rs(got, host_rs_inputs(n, count, "int32_pm2p20", seed), "int32", 0)
+
+
+def test_workload2_ag_bf16_n24():
+    n, count, seed = 24, 32768, 0x5041542
+    st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, count, "bfloat16")
+    assert info["slot_dims"] <= 5 and info["steps"] == 5  # ceil(log2 24)
+    got, host_in = run_ag(n, count, "bfloat16", seed)
+    np.testing.assert_array_equal(got, D.allgather(host_in))
+
+
+@pytest.mark.parametrize("mode", ["persistent", "graph"])
+def test_workload3_rs_f32_n64(mode):
+    n, count, seed = 64, 262144, 0x5041543
+    rng = np.random.default_rng(3)
+    sample = np.unique(np.concatenate([[0, 1, 2, 3, 1023, 1024, count - 1],
+                                       rng.integers(0, count, 4000)]))
+    got = run_rs(n, count, "float32", seed, mode=mode, sample=sample)
+    host_in = host_rs_inputs(n, count, "f32_normal", seed, sample)
+    check_rs(got, host_in, "float32", oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
+
+
+def test_workload4_small_chunks_n1000():
+    n, count, seed = 1000, 64, 0x5041544
+    st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, count, "float32")
+    assert info["steps"] == 10
+    got, host_in = run_ag(n, count, "float32", seed, dist="f32_pm1")
+    assert (got == host_in[None, :, :]).all()
+    # reduce-scatter: all 64 positions against the plain sum, 8 against the PAT order
+    got = run_rs(n, count, "float32", seed + 100, dist="f32_pm1")
+    dev_in = host_rs_inputs(n, count, "f32_pm1", seed + 100)
+    cols = np.array([0, 1, 7, 8, 31, 32, 62, 63])
+    pat_ref, _ = opat.reducescatter(np.ascontiguousarray(dev_in[:, :, cols]), opat.ceil_log2(n) - 1, "float32")
+    assert (got[:, cols].view(np.uint32) == pat_ref.view(np.uint32)).all()
+    exact = D.reducescatter_sum(dev_in, "float32")
+    scale = D.reducescatter_abs_sum(dev_in, "float32")
+    assert (np.abs(got.astype(np.float64) - exact) <= 1e-5 * scale).all()
+
+
+def test_workload5_rs_bf16_n128_full_size():
+    n, count, seed = 128, 2 * MIB, 0x5041545
+    rng = np.random.default_rng(5)
+    sample = np.unique(np.concatenate([[0, 1, 7, 8, 2047, 2048, count - 8, count - 1],
+                                       rng.integers(0, count, 1500)]))
+    got = run_rs(n, count, "bfloat16", seed, sample=sample)
+    torch.cuda.empty_cache()
+    host_in = host_rs_inputs(n, count, "bf16_normal", seed, sample)
+    check_rs(got, host_in, "bfloat16", oracle_t(pat.PAT_REDUCESCATTER, n, count, "bfloat16"))
+    pat.check(pat.pat_finalize())
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# Sweeps: rank counts, ragged sizes, budgets (aggregation levels, pieces), modes
+# ---------------------------------------------------------------------------
+
+SWEEP_N = [2, 3, 5, 7, 8, 13, 16, 33]
+
+
+@pytest.mark.parametrize("n", SWEEP_N)
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+@pytest.mark.parametrize("count", [1, 17, 1000, 4104])
+def test_sweep_default_budget(n, dtype, count):
+    seed = 1000 * n + count
+    got, host_in = run_ag(n, count, dtype, seed)
+    np.testing.assert_array_equal(got, D.allgather(host_in))
+    got = run_rs(n, count, dtype, seed + 1)
+    check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+             oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+
+
+@pytest.mark.parametrize("n", [5, 8, 13, 33])
+@pytest.mark.parametrize("budget", [4096, 16384, 65536])
+@pytest.mark.parametrize("mode", ["persistent", "graph", "stream"])
+def test_sweep_budgets_and_modes(n, budget, mode):
+    count = 4104  # float32: 16416-byte chunks, so 4096 B forces pieces and a ragged last piece
+    pat.check(pat.pat_set_buffer_bytes(budget))
+    try:
+        for dtype in ("float32", "bfloat16"):
+            seed = 7 * n + budget
+            got, host_in = run_ag(n, count, dtype, seed, mode=mode)
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+            got = run_rs(n, count, dtype, seed + 1, mode=mode)
+            check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+
+
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+@pytest.mark.parametrize("n", [1, 6, 9])
+def test_in_place(n, dtype):
+    count = 1000
+    got, host_in = run_ag(n, count, dtype, 77 + n, inplace=True)
+    np.testing.assert_array_equal(got, D.allgather(host_in))
+    got = run_rs(n, count, dtype, 78 + n, inplace=True)
+    check_rs(got, host_rs_inputs(n, count, DIST[dtype], 78 + n), dtype,
+             oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+
+
+def test_repeated_calls_reuse_plan_and_tables():
+    """Same plan, different buffers on the second call (pointer tables re-uploaded)."""
+    for rep in range(3):
+        got, host_in = run_ag(12, 256, "float32", 500 + rep, mode=["persistent", "graph", "stream"][rep])
+        np.testing.assert_array_equal(got, D.allgather(host_in))
+        got = run_rs(12, 256, "float32", 600 + rep, mode=["persistent", "graph", "stream"][rep])
+        check_rs(got, host_rs_inputs(12, 256, "f32_normal", 600 + rep), "float32",
+                 oracle_t(pat.PAT_REDUCESCATTER, 12, 256, "float32"))

@@ -1,0 +1,175 @@
+"""The library's host schedule (C++) against the oracle's (Python), and a
+symbolic execution of the library's step tables, slot indices included.
+
+Integer work: every comparison is exact.  No GPU needed.
+"""
+
+import pytest
+
+from oracle import pat as opat
+from paper_2506_20252_amd import pat
+
+NS = list(range(1, 70)) + [100, 127, 128, 129, 255, 256, 257, 1000]
+
+
+def library_steps(coll, n, count, dtype):
+    st, steps, entries = pat.pat_plan_steps(coll, n, count, dtype)
+    assert st == pat.PAT_OK
+    out, j = [], 0
+    for d, k in steps:
+        out.append((d, [e[0] for e in entries[j:j + k]]))
+        j += k
+    return out, steps, entries
+
+
+def budget_for(n, t, chunk_bytes):
+    """A budget that makes the library choose aggregation level t."""
+    k = max(len(P) for _, P in opat.schedule(n, t))
+    return k * chunk_bytes
+
+
+@pytest.mark.parametrize("n", NS)
+def test_schedule_matches_oracle_all_levels(n):
+    L = opat.ceil_log2(n)
+    count = 64  # float32: 256-byte chunks
+    try:
+        for t in range(max(L, 1)):
+            pat.pat_set_buffer_bytes(budget_for(n, t, count * 4) if n > 1 else 1 << 20)
+            ag, _, _ = library_steps(pat.PAT_ALLGATHER, n, count, "float32")
+            rs, _, _ = library_steps(pat.PAT_REDUCESCATTER, n, count, "float32")
+            want_t = opat.aggregation_level(n, count * 4, pat.pat_get_buffer_bytes())
+            ref = opat.schedule(n, want_t)
+            assert ag == [(d, sorted(P)) for d, P in ref]
+            assert rs == [(d, sorted(P)) for d, P in reversed(ref)]
+            if n > 2:
+                assert want_t == t or len(opat.schedule(n, want_t)) == len(opat.schedule(n, t))
+    finally:
+        pat.pat_set_buffer_bytes(0)
+
+
+@pytest.mark.parametrize("n,count,dtype", [(6, 1024, "int32"), (24, 32768, "bfloat16"),
+                                           (64, 262144, "float32"), (1000, 64, "float32"),
+                                           (128, 2 << 20, "bfloat16"), (37, 5000, "float32")])
+def test_aggregation_level_matches_oracle(n, count, dtype):
+    for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+        st, info = pat.pat_plan_info(coll, n, count, dtype)
+        slot_bytes = count * (4 if (coll == pat.PAT_REDUCESCATTER or dtype != "bfloat16") else 2)
+        t = opat.aggregation_level(n, slot_bytes, pat.pat_get_buffer_bytes())
+        assert info["t"] == t
+        assert info["steps"] == len(opat.schedule(n, t))
+
+
+def children(n, pos, reach):
+    c, d = 0, reach // 2
+    while d >= 1:
+        if pos + d < n:
+            c += 1
+        d //= 2
+    return c
+
+
+def run_symbolic_allgather(n, steps, entries):
+    """Execute the library's all-gather table on symbols: slots hold
+    (chunk, forwards left), receive buffers record arrivals."""
+    slots = {}
+    got = [{r} for r in range(n)]
+    peak = 0
+    j = 0
+    for d, k in steps:
+        writes = []
+        for r in range(n):
+            for (p, a, b, _c) in entries[j:j + k]:
+                c = (r - p) % n
+                if a == -1:
+                    assert p == 0
+                else:
+                    held = slots.get((r, a))
+                    assert held is not None and held[0] == c and held[1] > 0, "read of a slot not holding the chunk"
+                    held[1] -= 1
+                peer = (r + d) % n
+                writes.append((peer, c, b, children(n, p + d, d)))
+        for peer, c, b, fwd in writes:
+            assert c not in got[peer], "chunk received twice"
+            got[peer].add(c)
+            if b >= 0:
+                old = slots.get((peer, b))
+                assert old is None or old[1] == 0, "slot overwritten before it was drained"
+                assert fwd > 0
+                slots[(peer, b)] = [c, fwd]
+            else:
+                assert fwd == 0, "a forwarding receiver got no slot"
+        live = {}
+        for (rank, _), v in slots.items():
+            if v[1] > 0:
+                live[rank] = live.get(rank, 0) + 1
+        peak = max([peak] + list(live.values()))
+        j += k
+    assert all(got[r] == set(range(n)) for r in range(n))
+    assert all(v[1] == 0 for v in slots.values())
+    return peak
+
+
+def run_symbolic_reducescatter(n, steps, entries):
+    """Execute the library's reduce-scatter table on formal sums (sets of
+    contributing ranks), checking every slot read and write."""
+    slots = {}   # (rank, slot) -> [tree, position, set of ranks]
+    root = {}    # rank -> set of ranks
+    top = 1 << (opat.ceil_log2(n) - 1)
+    j = 0
+    for d, k in steps:
+        ops = []
+        for r in range(n):
+            for (p, a, b, c) in entries[j:j + k]:
+                tree = (r - p) % n
+                child = (r + d) % n
+                if a == -1:
+                    assert children(n, p + d, d) == 0, "a non-leaf child sent its raw input"
+                    part = {child}
+                else:
+                    held = slots.get((child, a))
+                    assert held is not None and held[0] == tree and held[1] == p + d
+                    part = held[2]
+                    slots[(child, a)] = None  # drained
+                ops.append((r, p, tree, b, c, part))
+        for r, p, tree, b, c, part in ops:
+            if b == -1:
+                assert d == 1
+                own = {r}
+            elif b == -2:
+                assert p == 0 and r in root
+                own = root[r]
+            else:
+                held = slots.get((r, b))
+                assert held is not None and held[0] == tree and held[1] == p
+                own = held[2]
+            assert not (own & part), "a contribution counted twice"
+            total = own | part
+            if c in (-2, -3):
+                assert p == 0 and tree == r
+                assert (c == -3) == (d == top)
+                root[r] = total
+            else:
+                old = slots.get((r, c))
+                assert old is None or (old[0] == tree and old[1] == p), "live slot overwritten"
+                slots[(r, c)] = [tree, p, total]
+        j += k
+    assert all(root[r] == set(range(n)) for r in range(n))
+    assert all(v is None for v in slots.values())
+
+
+@pytest.mark.parametrize("n", list(range(2, 34)) + [47, 64, 100])
+def test_symbolic_execution_of_library_tables(n):
+    L = opat.ceil_log2(n)
+    try:
+        for t in range(L):
+            pat.pat_set_buffer_bytes(budget_for(n, t, 256))
+            _, steps, entries = library_steps(pat.PAT_ALLGATHER, n, 64, "float32")
+            peak = run_symbolic_allgather(n, steps, entries)
+            T = 1 << t
+            assert peak <= L * T
+            _, steps, entries = library_steps(pat.PAT_REDUCESCATTER, n, 64, "float32")
+            run_symbolic_reducescatter(n, steps, entries)
+            st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, 64, "float32")
+            assert info["slot_dims"] <= L and info["slot_chunks_per_rank"] <= L * T
+    finally:
+        pat.pat_set_buffer_bytes(0)
