@@ -80,9 +80,11 @@ typedef enum {
    * (PAT_PERSISTENT_BLOCKS_PER_CU overrides) so that it is co-resident. */
   PAT_EXEC_PERSISTENT = 0,
   /* One kernel per step, captured once per plan (and vector width) into a
-   * HIP graph and replayed.  The default. */
+   * HIP graph and replayed. */
   PAT_EXEC_GRAPH = 1,
-  /* One kernel per step, launched directly on the stream. */
+  /* One kernel per step, launched directly on the stream.  The default: as
+   * fast as the graph for large operations, and without the graph launch's
+   * fixed cost for small ones. */
   PAT_EXEC_STREAM = 2
 } pat_exec_mode_t;
 
@@ -122,7 +124,7 @@ pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbuf
 pat_status_t pat_set_buffer_bytes(size_t bytes_per_slot);
 size_t pat_get_buffer_bytes(void);
 
-/* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_GRAPH, or the
+/* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_STREAM, or the
  * PAT_EXEC_MODE environment variable (persistent | graph | stream). */
 pat_status_t pat_set_exec_mode(int mode);
 int pat_get_exec_mode(void);

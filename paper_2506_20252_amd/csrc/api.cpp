@@ -42,9 +42,9 @@ int mode_now() {
   if (g_mode >= 0) return g_mode;
   if (const char* e = std::getenv("PAT_EXEC_MODE")) {
     if (!std::strcmp(e, "persistent")) return PAT_EXEC_PERSISTENT;
-    if (!std::strcmp(e, "stream")) return PAT_EXEC_STREAM;
+    if (!std::strcmp(e, "graph")) return PAT_EXEC_GRAPH;
   }
-  return PAT_EXEC_GRAPH;
+  return PAT_EXEC_STREAM;
 }
 
 uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }

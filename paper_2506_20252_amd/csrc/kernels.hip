@@ -35,17 +35,43 @@
 
 #include "kernels.hpp"
 
+// Tuning knobs (compile time): vectors in flight per lane, and nontemporal
+// (streaming) loads and stores.
+#ifndef PAT_UNROLL
+#define PAT_UNROLL 2
+#endif
+#ifndef PAT_NONTEMPORAL
+#define PAT_NONTEMPORAL 1
+#endif
+
 namespace pat {
 namespace {
 
+// Native clang vectors (not HIP's wrapper structs), so that the nontemporal
+// builtins apply directly to the 128-bit loads and stores.
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Buffer addresses come from pointer tables, so the compiler cannot tell they
+// are global memory and would emit flat accesses; every data access goes
+// through an explicit global (address space 1) pointer instead.
+#define PAT_GLOBAL __attribute__((address_space(1)))
+
 template <typename T>
 __device__ __forceinline__ T ldg(const char* p) {
-  return *reinterpret_cast<const T*>(p);
+  const PAT_GLOBAL T* q = (const PAT_GLOBAL T*)(p);
+  if constexpr (PAT_NONTEMPORAL) return __builtin_nontemporal_load(q);
+  return *q;
 }
 
 template <typename T>
 __device__ __forceinline__ void stg(char* p, const T& v) {
-  *reinterpret_cast<T*>(p) = v;
+  PAT_GLOBAL T* q = (PAT_GLOBAL T*)(p);
+  if constexpr (PAT_NONTEMPORAL)
+    __builtin_nontemporal_store(v, q);
+  else
+    *q = v;
 }
 
 __device__ __forceinline__ int wrap_add(int a, int b, int n) {
@@ -168,58 +194,41 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-struct F8 {
-  float4 lo, hi;
-};
-
 struct TI32V {
-  using in_t = uint4;
-  using acc_t = uint4;
+  using in_t = v4u;
+  using acc_t = v4u;
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
-  static constexpr int kUnroll = 4;
+  static constexpr int kUnroll = PAT_UNROLL;
   __device__ static acc_t widen(const in_t& x) { return x; }
   __device__ static in_t narrow(const acc_t& x) { return x; }
-  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
-    return make_uint4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-  }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) { return a + b; }  // wraps
 };
 
 struct TF32V {
-  using in_t = float4;
-  using acc_t = float4;
+  using in_t = v4f;
+  using acc_t = v4f;
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
-  static constexpr int kUnroll = 4;
+  static constexpr int kUnroll = PAT_UNROLL;
   __device__ static acc_t widen(const in_t& x) { return x; }
   __device__ static in_t narrow(const acc_t& x) { return x; }
-  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
-    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-  }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) { return a + b; }
 };
 
 struct TB16V {
-  using in_t = uint4;  // 8 bf16, element 2j in the low half of word j
-  using acc_t = F8;
+  using in_t = v2u;  // 4 bf16, element 2j in the low half of word j
+  using acc_t = v4f;
   static constexpr int kInElem = 2;
   static constexpr bool kSeparateRoot = true;
-  static constexpr int kUnroll = 2;
+  static constexpr int kUnroll = 2 * PAT_UNROLL;  // 8-byte input vectors: same bytes in flight
   __device__ static acc_t widen(const in_t& x) {
-    F8 r;
-    r.lo = make_float4(bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y));
-    r.hi = make_float4(bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w));
-    return r;
+    return v4f{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)};
   }
   __device__ static in_t narrow(const acc_t& a) {
-    return make_uint4(bf16_rne(a.lo.x) | (bf16_rne(a.lo.y) << 16), bf16_rne(a.lo.z) | (bf16_rne(a.lo.w) << 16),
-                      bf16_rne(a.hi.x) | (bf16_rne(a.hi.y) << 16), bf16_rne(a.hi.z) | (bf16_rne(a.hi.w) << 16));
+    return v2u{bf16_rne(a.x) | (bf16_rne(a.y) << 16), bf16_rne(a.z) | (bf16_rne(a.w) << 16)};
   }
-  __device__ static acc_t add(const acc_t& a, const acc_t& b) {
-    F8 r;
-    r.lo = make_float4(a.lo.x + b.lo.x, a.lo.y + b.lo.y, a.lo.z + b.lo.z, a.lo.w + b.lo.w);
-    r.hi = make_float4(a.hi.x + b.hi.x, a.hi.y + b.hi.y, a.hi.z + b.hi.z, a.hi.w + b.hi.w);
-    return r;
-  }
+  __device__ static acc_t add(const acc_t& a, const acc_t& b) { return a + b; }
 };
 
 struct TI32S {
@@ -448,7 +457,7 @@ hipError_t capacity_t(int* blocks) {
   return hipSuccess;
 }
 
-using AgV = AgOp<uint4, 4>;
+using AgV = AgOp<v4u, PAT_UNROLL>;
 using Ag4 = AgOp<uint32_t, 4>;
 using Ag2 = AgOp<uint16_t, 4>;
 
@@ -472,8 +481,8 @@ int variant_in_bytes(Variant v) {
   switch (v) {
     case kAgVec:
     case kRsI32Vec:
-    case kRsF32Vec:
-    case kRsB16Vec: return 16;
+    case kRsF32Vec: return 16;
+    case kRsB16Vec: return 8;
     case kAgS4:
     case kRsI32S:
     case kRsF32S: return 4;

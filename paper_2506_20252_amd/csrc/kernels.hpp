@@ -9,7 +9,10 @@
 
 namespace pat {
 
-constexpr int kThreads = 256;  // workgroup size: 4 wavefronts of 64
+#ifndef PAT_THREADS
+#define PAT_THREADS 256
+#endif
+constexpr int kThreads = PAT_THREADS;  // workgroup size, a multiple of the 64-lane wavefront
 
 // Everything a step kernel needs, passed by value (device pointers only).
 struct KCtx {
@@ -39,7 +42,7 @@ enum Variant : int {
   kAgS2,        // all-gather, 2-byte elements
   kRsI32Vec,
   kRsF32Vec,
-  kRsB16Vec,    // bf16 in, float32 partials
+  kRsB16Vec,    // bf16 in (4 per vector), float32 partials
   kRsI32S,
   kRsF32S,
   kRsB16S,

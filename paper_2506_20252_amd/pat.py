@@ -123,9 +123,16 @@ def _addr(b):
     return int(b.data_ptr()) if hasattr(b, "data_ptr") else int(b)
 
 
-def _ptr_array(bufs):
+def pointer_array(bufs):
+    """A ctypes array of device addresses, to build once and pass on every call
+    (the entry points accept it as is)."""
+    if isinstance(bufs, ctypes.Array):
+        return bufs
     vals = [_addr(b) for b in bufs]
     return (ctypes.c_void_p * max(len(vals), 1))(*vals)
+
+
+_ptr_array = pointer_array
 
 
 def _stream(stream):

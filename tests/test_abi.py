@@ -73,7 +73,7 @@ def test_argument_errors_before_any_device_call():
 def test_settings_roundtrip():
     assert pat.pat_set_exec_mode(5) == pat.PAT_ERR_INVALID_ARGUMENT
     old = pat.pat_get_exec_mode()
-    assert pat.pat_set_exec_mode("stream") == pat.PAT_OK and pat.pat_get_exec_mode() == pat.PAT_EXEC_STREAM
+    assert pat.pat_set_exec_mode("graph") == pat.PAT_OK and pat.pat_get_exec_mode() == pat.PAT_EXEC_GRAPH
     assert pat.pat_set_exec_mode(old) == pat.PAT_OK
     assert pat.pat_set_buffer_bytes(1 << 20) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 1 << 20
     assert pat.pat_set_buffer_bytes(0) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 8 << 20
