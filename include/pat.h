@@ -104,8 +104,9 @@ pat_status_t pat_allgather(const void* const* sendbufs, void* const* recvbufs, s
  * "Conversion to reduce-scatter operations"):
  *   recvbufs[R][i] = sum over x of sendbufs[x][R * count + i]   for i < count.
  *   sendbufs[x]: nranks * count elements.   recvbufs[R]: `count` elements.
- * Summation order: the reversed binomial tree of chunk R rooted at rank R,
- * children added nearest first; it does not depend on the buffer budget.
+ * Summation order: the reversed binomial tree of chunk R rooted at rank R;
+ * with the far-first linear order children are added nearest first and the
+ * order does not depend on the buffer budget.
  * In place: recvbufs[r] == sendbufs[r] + r * count.
  * count == 0: PAT_OK, nothing is launched.  nranks == 1: a plain copy.
  */
@@ -123,6 +124,19 @@ pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbuf
  */
 pat_status_t pat_set_buffer_bytes(size_t bytes_per_slot);
 size_t pat_get_buffer_bytes(void);
+
+/*
+ * Order of the linear part inside the T parallel sub-trees (section "The PAT
+ * algorithm"): far-first, the paper's main schedule and the default, or
+ * close-first, the alternative the paper allows.  Both drain every slot before
+ * its distance is used again, so both keep <= T chunks per slot; the step
+ * count is the same.  The reduce-scatter summation order follows the chosen
+ * walk.  Default: far-first, or the PAT_LINEAR_ORDER environment variable
+ * (far | close).  Affects plans created afterwards.
+ */
+typedef enum { PAT_LINEAR_FAR_FIRST = 0, PAT_LINEAR_CLOSE_FIRST = 1 } pat_linear_order_t;
+pat_status_t pat_set_linear_order(int order);
+int pat_get_linear_order(void);
 
 /* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_STREAM, or the
  * PAT_EXEC_MODE environment variable (persistent | graph | stream). */
@@ -166,7 +180,8 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
  *   pos[j]   tree position p (all-gather: the sender; reduce-scatter: the receiver);
  *   a[j], b[j], c[j]  slot indices (chunk entries of a rank's slot area) or markers:
  *     all-gather:     a = source slot or -1 (own send buffer),
- *                     b = slot written at the receiver or -1 (receive buffer only);
+ *                     b = slot written at the receiver or -1 (receive buffer only),
+ *                     c = -1 (unused);
  *     reduce-scatter: a = child's slot or -1 (child's raw input),
  *                     b = own accumulator slot, -1 (own raw input), -2 (root accumulator),
  *                     c = destination slot, -2 (root accumulator), -3 (root, last receive).

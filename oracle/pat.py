@@ -117,7 +117,25 @@ def far_first_walk(span: int):
     return order
 
 
-def schedule(nranks: int, t: int):
+def close_first_walk(span: int):
+    """The other linear order the paper allows (section "The PAT algorithm"):
+    from each node the nearest child first, then farther ones, each child's
+    whole sub-tree right after the edge that reached it (so each buffer is
+    still drained before its dimension is used again)."""
+    order = []
+
+    def walk(q, w):
+        d = 1
+        while d < w:
+            order.append((q, d))
+            walk(q + d, d)
+            d *= 2
+
+    walk(0, span)
+    return order
+
+
+def schedule(nranks: int, t: int, order: str = "far"):
     """All-gather steps for N ranks and T = 2^t parallel sub-trees.
 
     Returns a list of (d, P): at that step every rank r sends, for each tree
@@ -125,16 +143,20 @@ def schedule(nranks: int, t: int):
     the relative tree is given a step: the top t dimensions (d >= M) get one
     fully aggregated step each, farthest first; an edge below the top belongs
     to sub-tree p // M and is sent at the position its relative edge
-    (p mod M, d) has in the far-first walk of a span-M sub-tree.  Positions that
+    (p mod M, d) has in the linear walk of a span-M sub-tree: far-first
+    (order="far", the default) or close-first (order="close").  Positions that
     a truncated tree lacks simply send nothing; a step left with no edge does
     not exist.
     """
+    if order not in ("far", "close"):
+        raise ValueError(order)
     if nranks <= 1:
         return []
     L = ceil_log2(nranks)
     t = max(0, min(t, L - 1))
     M = 1 << (L - t)
-    walk_index = {edge: i for i, edge in enumerate(far_first_walk(M))}
+    walk = far_first_walk(M) if order == "far" else close_first_walk(M)
+    walk_index = {edge: i for i, edge in enumerate(walk)}
     groups = {}
     for p, _child, d in tree_edges(nranks):
         if d >= M:
@@ -173,7 +195,7 @@ def children(nranks: int, p: int, reach: int) -> int:
     return n
 
 
-def allgather(inputs: np.ndarray, t: int):
+def allgather(inputs: np.ndarray, t: int, order: str = "far"):
     """Execute the all-gather steps on per-rank data.
 
     inputs: (N, m) -- rank x's send buffer.  Returns (recv, stats): recv is
@@ -195,7 +217,7 @@ def allgather(inputs: np.ndarray, t: int):
         have[r, r] = True
     buf = [dict() for _ in range(N)]  # rank -> {(d, chunk): [data, forwards left]}
     peak = {}  # d -> most chunks any rank held for dimension d at once
-    steps = schedule(N, t)
+    steps = schedule(N, t, order)
     for d, P in steps:
         messages = []
         for r in range(N):
@@ -259,7 +281,7 @@ def _add(a, b, dtype):
     return (a + b).astype(np.float32)  # float32 + float32, one rounding
 
 
-def reducescatter(inputs: np.ndarray, t: int, dtype: str):
+def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far"):
     """Execute the reduce-scatter steps (reversed trees) on per-rank data.
 
     inputs: (N, N, m) -- inputs[x][c] is rank x's contribution to chunk c.
@@ -283,7 +305,7 @@ def reducescatter(inputs: np.ndarray, t: int, dtype: str):
     root = [None] * N   # rank -> its own chunk's running sum
     acc = [dict() for _ in range(N)]  # rank -> {(d, chunk): partial}
     peak = {}
-    steps = list(reversed(schedule(N, t)))
+    steps = list(reversed(schedule(N, t, order)))
     for d, P in steps:
         arriving = []
         for r in range(N):

@@ -27,6 +27,7 @@ std::mutex g_mu;
 size_t g_budget = 0;     // 0: default
 int g_mode = -1;         // -1: environment / default
 uint32_t g_timeout_us = 0;  // 0: default
+int g_order = -1;           // -1: environment / default (far-first)
 std::atomic<int> g_last_hip{0};
 
 size_t budget_now() {
@@ -45,6 +46,13 @@ int mode_now() {
     if (!std::strcmp(e, "graph")) return PAT_EXEC_GRAPH;
   }
   return PAT_EXEC_STREAM;
+}
+
+int order_now() {
+  if (g_order >= 0) return g_order;
+  if (const char* e = std::getenv("PAT_LINEAR_ORDER"))
+    if (!std::strcmp(e, "close")) return pat::kCloseFirst;
+  return pat::kFarFirst;
 }
 
 uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }
@@ -111,7 +119,7 @@ struct Plan {
   }
 };
 
-using PlanKey = std::tuple<int, int, int64_t, int, size_t, int>;  // coll, N, count, dtype, budget, device
+using PlanKey = std::tuple<int, int, int64_t, int, size_t, int, int>;  // coll, N, count, dtype, budget, order, device
 std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
 
 // Launch-level steps for one vector width: every schedule step of every piece.
@@ -155,10 +163,10 @@ pat::Variant variant_for(int coll, pat_dtype_t dt, bool vec) {
   }
 }
 
-pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int device,
+pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int device,
                          Plan** out) {
   auto p = std::make_unique<Plan>();
-  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, &p->desc)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &p->desc)) return PAT_ERR_INVALID_ARGUMENT;
   pat::PlanDesc& d = p->desc;
   p->device = device;
   const bool vec_ok = (count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
@@ -219,7 +227,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
     }
   }
   *out = p.get();
-  g_plans[PlanKey(coll, N, count, (int)dt, budget, device)] = std::move(p);
+  g_plans[PlanKey(coll, N, count, (int)dt, budget, order, device)] = std::move(p);
   return PAT_OK;
 }
 
@@ -283,12 +291,13 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   int device = 0;
   HIP_TRY(hipGetDevice(&device));
   const size_t budget = budget_now();
+  const int order = order_now();
   Plan* plan = nullptr;
-  auto it = g_plans.find(PlanKey(coll, N, (int64_t)count, (int)dt, budget, device));
+  auto it = g_plans.find(PlanKey(coll, N, (int64_t)count, (int)dt, budget, order, device));
   if (it != g_plans.end()) {
     plan = it->second.get();
   } else {
-    const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, device, &plan);
+    const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, order, device, &plan);
     if (s != PAT_OK) return s;
   }
   vec = vec && plan->has_vec;
@@ -389,11 +398,13 @@ pat_status_t describe(int coll, int N, size_t count, pat_dtype_t dt, pat::PlanDe
   if (dt != PAT_INT32 && dt != PAT_FLOAT32 && dt != PAT_BFLOAT16) return PAT_ERR_UNSUPPORTED;
   if (count > (size_t(1) << 40)) return PAT_ERR_INVALID_ARGUMENT;
   size_t budget;
+  int order;
   {
     std::lock_guard<std::mutex> lock(g_mu);
     budget = budget_now();
+    order = order_now();
   }
-  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, d)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, order, d)) return PAT_ERR_INVALID_ARGUMENT;
   return PAT_OK;
 }
 
@@ -433,6 +444,18 @@ pat_status_t pat_set_exec_mode(int mode) {
 int pat_get_exec_mode(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   return mode_now();
+}
+
+pat_status_t pat_set_linear_order(int order) {
+  if (order != PAT_LINEAR_FAR_FIRST && order != PAT_LINEAR_CLOSE_FIRST) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_order = order;
+  return PAT_OK;
+}
+
+int pat_get_linear_order(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  return order_now();
 }
 
 pat_status_t pat_set_barrier_timeout_us(uint32_t microseconds) {

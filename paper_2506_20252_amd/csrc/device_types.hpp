@@ -13,7 +13,8 @@ enum : int32_t {
 };
 
 // One chunk-edge of a step, relative to the acting rank r (16 bytes).
-//   all-gather:     p = sender position;   a = source slot | kUser;   b = receiver slot | kUser (none)
+//   all-gather:     p = sender position;   a = source slot | kUser;   b = receiver slot | kUser (none);
+//                   c = kUser (unused)
 //   reduce-scatter: p = receiver position; a = child slot | kUser (child's input);
 //                   b = own accumulator slot | kUser (own input) | kRoot;
 //                   c = destination slot | kRoot | kRootFinal

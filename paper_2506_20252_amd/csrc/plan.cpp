@@ -35,7 +35,16 @@ static void far_first_walk(int span, std::vector<std::pair<int, int>>* out) {
   }
 }
 
-Schedule make_schedule(int N, int t) {
+// Close-first pre-order walk: from a node, the nearest child first, each
+// child's whole sub-tree right after the edge that reached it.
+static void close_first_walk(int q, int span, std::vector<std::pair<int, int>>* out) {
+  for (int d = 1; d < span; d <<= 1) {
+    out->emplace_back(q, d);
+    close_first_walk(q + d, d, out);
+  }
+}
+
+Schedule make_schedule(int N, int t, int order) {
   Schedule s;
   s.N = N;
   if (N <= 1) return s;
@@ -53,7 +62,10 @@ Schedule make_schedule(int N, int t) {
   }
   // Linear part: the walk of one span-M sub-tree, taken by all T at once.
   std::vector<std::pair<int, int>> walk;
-  far_first_walk(s.M, &walk);
+  if (order == kCloseFirst)
+    close_first_walk(0, s.M, &walk);
+  else
+    far_first_walk(s.M, &walk);
   for (const auto& [q, d] : walk) {
     StepSpec st{d, 0, (int32_t)s.pos.size()};
     for (int b = 0; b < s.T; ++b) {
@@ -109,10 +121,12 @@ SlotMap make_slot_map(int N, int L, int M) {
 
 static int elem_bytes(int dtype) { return dtype == 2 ? 2 : 4; }
 
-bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, PlanDesc* out) {
+bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out) {
   if (coll < 0 || coll > 1 || N < 1 || count < 0 || dtype < 0 || dtype > 2) return false;
+  if (order != kFarFirst && order != kCloseFirst) return false;
   PlanDesc d;
   d.coll = coll;
+  d.order = order;
   d.N = N;
   d.dtype = dtype;
   d.count = count;
@@ -124,11 +138,11 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, Pl
   if (N > 1) {
     const int L = ceil_log2(N);
     for (t = L - 1; t > 0; --t) {
-      const Schedule s = make_schedule(N, t);
+      const Schedule s = make_schedule(N, t, order);
       if (double(max_chunks_per_step(s)) * c_slot <= double(budget)) break;
     }
   }
-  d.sched = make_schedule(N, t);
+  d.sched = make_schedule(N, t, order);
   d.max_k = max_chunks_per_step(d.sched);
 
   // A chunk larger than the budget is processed in pieces (T = 1 then).
@@ -145,7 +159,6 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, Pl
   const int M = d.sched.M;
   d.slots = make_slot_map(N, d.sched.L, M);
   const auto& S = d.sched;
-  const int top_d = S.L > 0 ? 1 << (S.L - 1) : 0;
   if (coll == 0) {
     for (const auto& st : S.steps) {
       d.exec.push_back({st.d, st.k, (int32_t)d.entries.size()});
@@ -156,23 +169,36 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, Pl
         e.a = p == 0 ? kUser : d.slots.index(p);
         const int32_t to = d.slots.index(p + st.d);
         e.b = to >= 0 ? to : kUser;
-        e.c = 0;
+        e.c = kUser;  // unused by the all-gather
         if (p != 0 && e.a < 0) return false;  // a forwarding node always has a slot
         d.entries.push_back(e);
       }
     }
   } else {
+    // A receiver's first receive starts from its own input, and the root's
+    // last receive writes the receive buffer; which receives those are
+    // follows from the execution order (far-first: distance 1 first and the
+    // farthest distance last; close-first reverses the linear part).
+    std::vector<int32_t> first(N, -1), last(N, -1);
+    int32_t idx = 0;
+    for (auto it = S.steps.rbegin(); it != S.steps.rend(); ++it)
+      for (int j = 0; j < it->k; ++j, ++idx) {
+        const int p = S.pos[it->first + j];
+        if (first[p] < 0) first[p] = idx;
+        last[p] = idx;
+      }
+    idx = 0;
     for (auto it = S.steps.rbegin(); it != S.steps.rend(); ++it) {
       const auto& st = *it;
       d.exec.push_back({st.d, st.k, (int32_t)d.entries.size()});
-      for (int j = 0; j < st.k; ++j) {
+      for (int j = 0; j < st.k; ++j, ++idx) {
         const int p = S.pos[st.first + j];
         DevEntry e{};
         e.p = p;
         const int32_t child = d.slots.index(p + st.d);
         e.a = child >= 0 ? child : kUser;  // a leaf child sends its raw input
-        if (st.d == 1) {
-          e.b = kUser;  // first receive: start from the own input
+        if (first[p] == idx) {
+          e.b = kUser;
         } else if (p == 0) {
           e.b = kRoot;
         } else {
@@ -180,7 +206,7 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, Pl
           if (e.b < 0) return false;
         }
         if (p == 0) {
-          e.c = st.d == top_d ? kRootFinal : kRoot;
+          e.c = last[p] == idx ? kRootFinal : kRoot;
         } else {
           e.c = d.slots.index(p);
           if (e.c < 0) return false;

@@ -31,12 +31,18 @@ struct Schedule {
   std::vector<int32_t> pos;     // sender positions, step after step
 };
 
+// Linear order inside the parallel sub-trees (section "The PAT algorithm"):
+// far-first (the paper's main schedule) or close-first (the alternative it
+// allows).  Both are pre-order walks, so each slot is drained before its
+// distance is used again.
+enum LinearOrder : int { kFarFirst = 0, kCloseFirst = 1 };
+
 // Steps for N ranks and T = 2^t parallel sub-trees (section "The PAT
 // algorithm"): the top t distances fully aggregated, farthest first; then a
-// far-first pre-order walk of a span-M sub-tree (M = 2^(L - t)), every walk
-// edge taken in all T sub-trees at once.  Edges a truncated tree lacks are
-// dropped, and so is a step left empty.
-Schedule make_schedule(int N, int t);
+// pre-order walk of a span-M sub-tree (M = 2^(L - t)) in the given linear
+// order, every walk edge taken in all T sub-trees at once.  Edges a truncated
+// tree lacks are dropped, and so is a step left empty.
+Schedule make_schedule(int N, int t, int order = kFarFirst);
 
 int max_chunks_per_step(const Schedule& s);
 
@@ -60,6 +66,7 @@ SlotMap make_slot_map(int N, int L, int M);
 
 struct PlanDesc {
   int coll = 0;        // 0 all-gather, 1 reduce-scatter
+  int order = kFarFirst;
   int N = 0;
   int dtype = 0;
   int64_t count = 0;
@@ -76,7 +83,7 @@ struct PlanDesc {
 };
 
 // Budget in bytes per slot.  Returns false for unsupported arguments.
-bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, PlanDesc* out);
+bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out);
 
 // Algorithmic memory bytes of one operation (read + written by the steps):
 // all-gather: per chunk-edge, read C, write C to the receiver's buffer, write

@@ -40,10 +40,15 @@ PAT_EXEC_GRAPH = 1
 PAT_EXEC_STREAM = 2
 MODES = {"persistent": PAT_EXEC_PERSISTENT, "graph": PAT_EXEC_GRAPH, "stream": PAT_EXEC_STREAM}
 
+PAT_LINEAR_FAR_FIRST = 0
+PAT_LINEAR_CLOSE_FIRST = 1
+ORDERS = {"far": PAT_LINEAR_FAR_FIRST, "close": PAT_LINEAR_CLOSE_FIRST}
+
 # Every function include/pat.h declares.
 EXPORTS = (
     "pat_allgather", "pat_reducescatter", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
-    "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_barrier_timeout_us", "pat_plan_info",
+    "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
+    "pat_set_barrier_timeout_us", "pat_plan_info",
     "pat_plan_steps", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
     "pat_finalize",
 )
@@ -90,6 +95,8 @@ def lib():
             "pat_get_buffer_bytes": ([], ctypes.c_size_t),
             "pat_set_exec_mode": ([ctypes.c_int], ctypes.c_int),
             "pat_get_exec_mode": ([], ctypes.c_int),
+            "pat_set_linear_order": ([ctypes.c_int], ctypes.c_int),
+            "pat_get_linear_order": ([], ctypes.c_int),
             "pat_set_barrier_timeout_us": ([ctypes.c_uint32], ctypes.c_int),
             "pat_plan_info": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                                ctypes.POINTER(pat_plan_info_t)], ctypes.c_int),
@@ -167,6 +174,14 @@ def pat_set_exec_mode(mode):
 
 def pat_get_exec_mode():
     return int(lib().pat_get_exec_mode())
+
+
+def pat_set_linear_order(order):
+    return lib().pat_set_linear_order(ORDERS[order] if isinstance(order, str) else int(order))
+
+
+def pat_get_linear_order():
+    return int(lib().pat_get_linear_order())
 
 
 def pat_set_barrier_timeout_us(microseconds):

@@ -270,3 +270,54 @@ def test_repeated_calls_reuse_plan_and_tables():
         got = run_rs(12, 256, "float32", 600 + rep, mode=["persistent", "graph", "stream"][rep])
         check_rs(got, host_rs_inputs(12, 256, "f32_normal", 600 + rep), "float32",
                  oracle_t(pat.PAT_REDUCESCATTER, 12, 256, "float32"))
+
+
+@pytest.mark.parametrize("n", [6, 13, 33])
+@pytest.mark.parametrize("budget", [4096, 65536])
+def test_close_first_linear_order(n, budget):
+    count = 4104
+    pat.check(pat.pat_set_buffer_bytes(budget))
+    pat.check(pat.pat_set_linear_order("close"))
+    try:
+        for dtype in ("float32", "bfloat16", "int32"):
+            seed = 31 * n + budget
+            got, host_in = run_ag(n, count, dtype, seed)
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+            got = run_rs(n, count, dtype, seed + 1)
+            host = host_rs_inputs(n, count, DIST[dtype], seed + 1)
+            if dtype == "int32":
+                np.testing.assert_array_equal(got, D.reducescatter_sum(host, "int32"))
+                continue
+            t = oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype)
+            pat_ref, _ = opat.reducescatter(host, t, dtype, "close")
+            width = np.uint32 if dtype == "float32" else np.uint16
+            assert (got.view(width) == pat_ref.view(width)).all()
+    finally:
+        pat.check(pat.pat_set_linear_order("far"))
+        pat.check(pat.pat_set_buffer_bytes(0))
+
+
+def test_persistent_barrier_timeout_is_reported_and_recovers():
+    """Failure handling forced from the host: a 1 us limit on the persistent
+    kernel's own bounded barrier wait.  Every workgroup still exits; the
+    timeout is reported, and the next operation on the same plan is correct."""
+    n, count, seed = 64, 262144, 0x77
+    pat.check(pat.pat_set_barrier_timeout_us(1))
+    try:
+        dev = torch.device("cuda:0")
+        send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+        fill_ranks(send, "f32_normal", seed)
+        recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+        pat.check(pat.pat_set_exec_mode("persistent"))
+        stream = torch.cuda.current_stream()
+        log("[gpu] persistent reduce-scatter with a 1 us barrier limit")
+        pat.check(pat.pat_reducescatter(list(send), list(recv), count, "float32", pat.PAT_SUM, n, stream))
+        assert pat.pat_check_device_status(stream) == pat.PAT_ERR_TIMEOUT
+        assert pat.pat_check_device_status(stream) == pat.PAT_OK  # reported once, then cleared
+        del send, recv
+    finally:
+        pat.check(pat.pat_set_barrier_timeout_us(0))
+    sample = np.array([0, 5, 4096, count - 1])
+    got = run_rs(n, count, "float32", seed, mode="persistent", sample=sample)
+    check_rs(got, host_rs_inputs(n, count, "f32_normal", seed, sample), "float32",
+             oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))

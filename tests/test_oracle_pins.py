@@ -422,3 +422,47 @@ def test_planted_near_first_walk_is_caught(monkeypatch):
     x = RNG.standard_normal((8, 8, 64)).astype(np.float32)
     out, _ = pat.reducescatter(x, 0, "float32")
     assert not (out.view(np.uint32) == closed_form(x, "float32").view(np.uint32)).all()
+
+
+# --------------------------------------------------------------------------
+# The close-first linear order (section "The PAT algorithm": the alternative
+# schedule that sends close first, then far)
+# --------------------------------------------------------------------------
+
+def test_close_first_n8_aggregation_two():
+    # reading (close-first pre-order walk): same edges per step as far-first,
+    # the linear part taken nearest child first
+    s = pat.schedule(8, 1, "close")
+    assert s == [(4, [0]), (1, [0, 4]), (2, [0, 4]), (1, [2, 6])]
+    assert sorted(map(str, s)) == sorted(map(str, pat.schedule(8, 1, "far")))
+
+
+@pytest.mark.parametrize("n", list(range(2, 34)) + [47, 64])
+def test_close_first_invariants(n):
+    L = pat.ceil_log2(n)
+    for t in range(L):
+        T = 1 << t
+        far, close = pat.schedule(n, t, "far"), pat.schedule(n, t, "close")
+        assert len(far) == len(close)  # same step count
+        assert sorted(map(str, far)) == sorted(map(str, close))  # same steps, other order
+        x = np.arange(n, dtype=np.int32).reshape(n, 1)
+        recv, st = pat.allgather(x, t, "close")  # exactly once, checked inside
+        assert (recv[:, :, 0] == np.arange(n)[None, :]).all()
+        assert all(v <= T for v in st["peak_per_dim"].values())
+        y = RNG.integers(-2**31, 2**31, size=(n, n, 3), dtype=np.int64).astype(np.int32)
+        out, st2 = pat.reducescatter(y, t, "int32", "close")
+        assert (out == D.reducescatter_sum(y, "int32")).all()
+        assert all(v <= T for v in st2["peak_per_dim"].values())
+
+
+@pytest.mark.parametrize("n", [6, 24, 33])
+def test_close_first_fp32_error_bound(n):
+    x = RNG.standard_normal((n, n, 129)).astype(np.float32)
+    L = pat.ceil_log2(n)
+    exact = D.reducescatter_sum(x, "float32")
+    scale = D.reducescatter_abs_sum(x, "float32")
+    gamma = L * 2.0 ** -24 / (1 - L * 2.0 ** -24)
+    for t in range(L):
+        out, _ = pat.reducescatter(x, t, "float32", "close")
+        # each term still passes through at most L adds (the tree's depth)
+        assert (np.abs(out.astype(np.float64) - exact) <= gamma * scale).all()

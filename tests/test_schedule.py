@@ -28,23 +28,26 @@ def budget_for(n, t, chunk_bytes):
     return k * chunk_bytes
 
 
+@pytest.mark.parametrize("order", ["far", "close"])
 @pytest.mark.parametrize("n", NS)
-def test_schedule_matches_oracle_all_levels(n):
+def test_schedule_matches_oracle_all_levels(n, order):
     L = opat.ceil_log2(n)
     count = 64  # float32: 256-byte chunks
+    pat.check(pat.pat_set_linear_order(order))
     try:
         for t in range(max(L, 1)):
             pat.pat_set_buffer_bytes(budget_for(n, t, count * 4) if n > 1 else 1 << 20)
             ag, _, _ = library_steps(pat.PAT_ALLGATHER, n, count, "float32")
             rs, _, _ = library_steps(pat.PAT_REDUCESCATTER, n, count, "float32")
             want_t = opat.aggregation_level(n, count * 4, pat.pat_get_buffer_bytes())
-            ref = opat.schedule(n, want_t)
+            ref = opat.schedule(n, want_t, order)
             assert ag == [(d, sorted(P)) for d, P in ref]
             assert rs == [(d, sorted(P)) for d, P in reversed(ref)]
             if n > 2:
                 assert want_t == t or len(opat.schedule(n, want_t)) == len(opat.schedule(n, t))
     finally:
         pat.pat_set_buffer_bytes(0)
+        pat.pat_set_linear_order("far")
 
 
 @pytest.mark.parametrize("n,count,dtype", [(6, 1024, "int32"), (24, 32768, "bfloat16"),
@@ -114,12 +117,17 @@ def run_symbolic_reducescatter(n, steps, entries):
     contributing ranks), checking every slot read and write."""
     slots = {}   # (rank, slot) -> [tree, position, set of ranks]
     root = {}    # rank -> set of ranks
-    top = 1 << (opat.ceil_log2(n) - 1)
+    last_root = max(j for j, e in enumerate(entries) if e[0] == 0)
+    seen = set()  # positions that have received already (the same for every rank)
     j = 0
     for d, k in steps:
         ops = []
+        first = {}
+        for jj, (p, _a, _b, _c) in enumerate(entries[j:j + k]):
+            first[jj] = p not in seen
+            seen.add(p)
         for r in range(n):
-            for (p, a, b, c) in entries[j:j + k]:
+            for jj, (p, a, b, c) in enumerate(entries[j:j + k]):
                 tree = (r - p) % n
                 child = (r + d) % n
                 if a == -1:
@@ -130,10 +138,10 @@ def run_symbolic_reducescatter(n, steps, entries):
                     assert held is not None and held[0] == tree and held[1] == p + d
                     part = held[2]
                     slots[(child, a)] = None  # drained
-                ops.append((r, p, tree, b, c, part))
-        for r, p, tree, b, c, part in ops:
+                ops.append((r, p, tree, b, c, part, first[jj], j + jj == last_root))
+        for r, p, tree, b, c, part, is_first, is_last_root in ops:
+            assert (b == -1) == is_first, "own input must enter exactly at the first receive"
             if b == -1:
-                assert d == 1
                 own = {r}
             elif b == -2:
                 assert p == 0 and r in root
@@ -146,7 +154,7 @@ def run_symbolic_reducescatter(n, steps, entries):
             total = own | part
             if c in (-2, -3):
                 assert p == 0 and tree == r
-                assert (c == -3) == (d == top)
+                assert (c == -3) == is_last_root
                 root[r] = total
             else:
                 old = slots.get((r, c))
@@ -157,9 +165,11 @@ def run_symbolic_reducescatter(n, steps, entries):
     assert all(v is None for v in slots.values())
 
 
+@pytest.mark.parametrize("order", ["far", "close"])
 @pytest.mark.parametrize("n", list(range(2, 34)) + [47, 64, 100])
-def test_symbolic_execution_of_library_tables(n):
+def test_symbolic_execution_of_library_tables(n, order):
     L = opat.ceil_log2(n)
+    pat.check(pat.pat_set_linear_order(order))
     try:
         for t in range(L):
             pat.pat_set_buffer_bytes(budget_for(n, t, 256))
@@ -173,3 +183,4 @@ def test_symbolic_execution_of_library_tables(n):
             assert info["slot_dims"] <= L and info["slot_chunks_per_rank"] <= L * T
     finally:
         pat.pat_set_buffer_bytes(0)
+        pat.pat_set_linear_order("far")
