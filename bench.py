@@ -114,6 +114,57 @@ def cpu_baseline(wid, target_seconds, sample_inputs, m_cap):
             "seconds": round(elapsed, 2)}
 
 
+def small_size_latency(reps=200):
+    """The small-size regime: N = 1000 virtual ranks, 64 fp32 (256 B) per chunk,
+    U[-1, 1) from seed 0x5041544.  Microseconds per all-gather and per
+    reduce-scatter (HIP events around `reps` back-to-back operations), and the
+    step count beside log2 N and a ring's N - 1."""
+    import math
+
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    n, count, seed = 1000, 64, 0x5041544
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    out = {"workload": "N=1000 virtual ranks, 64 fp32 (256 B) per chunk, U[-1,1)", "log2_n": round(math.log2(n), 3),
+           "ring_steps": n - 1}
+    for coll in ("allgather", "reducescatter"):
+        if coll == "reducescatter":
+            send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+            recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+        else:
+            send = torch.empty((n, count), dtype=torch.float32, device=dev)
+            recv = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+        for x in range(n):
+            synth.fill(send[x], "f32_pm1", seed, x)
+        S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+        if coll == "reducescatter":
+            op = lambda: pat.pat_reducescatter(S, R, count, "float32", pat.PAT_SUM, n, stream)  # noqa: E731
+            code = pat.PAT_REDUCESCATTER
+        else:
+            op = lambda: pat.pat_allgather(S, R, count, "float32", n, stream)  # noqa: E731
+            code = pat.PAT_ALLGATHER
+        for _ in range(5):
+            pat.check(op())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            pat.check(op())
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pat.check(pat.pat_check_device_status(stream))
+        st, info = pat.pat_plan_info(code, n, count, "float32")
+        out[f"{coll}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+        out["steps"] = info["steps"]
+        del send, recv, S, R
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_probe(nbytes, reps):
     """A plain device-to-device copy of known size: reads and writes nbytes."""
     import torch
@@ -145,6 +196,7 @@ def main():
     ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-latency", action="store_true", help="skip the small-size latency figures")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: all virtual ranks are emulated on one GPU; runs on more than one GPU "
@@ -243,6 +295,8 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},
     }
+    if not args.no_latency:
+        out["small_size_latency"] = small_size_latency()
     if not args.no_cpu_baseline:
         # The oracle's inputs: the first m positions of every chunk of the
         # generator-filled send buffers (the collective only reads them).

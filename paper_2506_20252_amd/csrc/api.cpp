@@ -66,6 +66,16 @@ int blocks_per_cu_cap() {
   return 2;
 }
 
+// Loads stream (nontemporal) when an operation moves at least this many bytes;
+// smaller operations keep their data in the 256 MB Infinity Cache between
+// steps.  PAT_NT_LOADS=0/1 overrides.
+constexpr double kStreamingLoadBytes = 1e9;
+
+bool nt_loads_for(double alg_bytes) {
+  if (const char* e = std::getenv("PAT_NT_LOADS")) return e[0] == '1';
+  return alg_bytes >= kStreamingLoadBytes;
+}
+
 int elem_size(pat_dtype_t t) { return t == PAT_BFLOAT16 ? 2 : 4; }
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -98,7 +108,8 @@ struct Plan {
   hipEvent_t upload_done = nullptr;
   bool upload_pending = false;
   hipGraphExec_t graph[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};  // [vec][own_copy]
-  int capacity[pat::kNumVariants] = {};
+  int capacity[pat::kNumVariants][2] = {};
+  bool nt_loads = true;
   int cus = 0;
   int64_t clock_khz = 0;
 
@@ -173,6 +184,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   const pat::Variant vs = variant_for(coll, dt, false), vv = variant_for(coll, dt, true);
   if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
+  p->nt_loads = nt_loads_for(d.alg_bytes);
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
@@ -220,10 +232,10 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
     if (e[0] == '1') {
       std::fprintf(stderr,
                    "[pat] plan coll=%d N=%d count=%lld dtype=%d L=%d t=%d T=%d steps=%zu pieces=%d "
-                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d\n",
+                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d nt_loads=%d\n",
                    coll, N, (long long)count, (int)dt, d.sched.L, d.sched.t, d.sched.T, d.exec.size(),
                    d.pieces, d.max_k, d.slots.entries, (long long)(p->slot_rank_stride * N), d.alg_bytes,
-                   (int)p->has_vec);
+                   (int)p->has_vec, (int)p->nt_loads);
     }
   }
   *out = p.get();
@@ -354,19 +366,22 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   const auto& steps = plan->steps[vi];
   const int mode = mode_now();
   if (mode == PAT_EXEC_PERSISTENT) {
-    if (plan->capacity[var] == 0) HIP_TRY(pat::persistent_capacity(var, &plan->capacity[var]));
+    const bool nt = plan->nt_loads;
+    int& capacity = plan->capacity[var][nt ? 1 : 0];
+    if (capacity == 0) HIP_TRY(pat::persistent_capacity(var, nt, &capacity));
     int64_t most = 1;
     for (const auto& st : steps) most = std::max(most, st.items);
-    int64_t cap = plan->capacity[var];
+    int64_t cap = capacity;
     if (const int per_cu = blocks_per_cu_cap()) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));
     if (const char* e = std::getenv("PAT_DEBUG"))
       if (e[0] == '1')
         std::fprintf(stderr, "[pat] persistent launch: capacity=%d cus=%d grid=%d steps=%d\n",
-                     plan->capacity[var], plan->cus, grid, cx.nsteps);
-    HIP_TRY(pat::launch_persistent(var, cx, grid, stream));
+                     capacity, plan->cus, grid, cx.nsteps);
+    HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
   } else if (mode == PAT_EXEC_STREAM) {
-    for (size_t s = 0; s < steps.size(); ++s) HIP_TRY(pat::launch_step(var, cx, (int)s, steps[s].items, stream));
+    for (size_t s = 0; s < steps.size(); ++s)
+      HIP_TRY(pat::launch_step(var, plan->nt_loads, cx, (int)s, steps[s].items, stream));
   } else {
     hipGraphExec_t& exec = plan->graph[vi][cx.own_copy];
     if (!exec) {
@@ -375,7 +390,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
       hipGraph_t g = nullptr;
       hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
       for (size_t s = 0; e == hipSuccess && s < steps.size(); ++s)
-        e = pat::launch_step(var, cx, (int)s, steps[s].items, cs);
+        e = pat::launch_step(var, plan->nt_loads, cx, (int)s, steps[s].items, cs);
       const hipError_t e2 = hipStreamEndCapture(cs, &g);
       if (e == hipSuccess) e = e2;
       if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);

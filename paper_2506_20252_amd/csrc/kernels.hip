@@ -35,13 +35,20 @@
 
 #include "kernels.hpp"
 
-// Tuning knobs (compile time): vectors in flight per lane, and nontemporal
-// (streaming) loads and stores.
+// Tuning knobs (compile time): vectors in flight per lane, nontemporal
+// (streaming) stores, and the XCD-aware work-item order.
 #ifndef PAT_UNROLL
 #define PAT_UNROLL 2
 #endif
-#ifndef PAT_NONTEMPORAL
-#define PAT_NONTEMPORAL 1
+// Stores always stream; the loads' hint is chosen per plan (launch argument).
+#ifndef PAT_NT_STORES
+#define PAT_NT_STORES 1
+#endif
+// 1: workgroup b of a step takes work item (b % 8) * ceil(items / 8) + b / 8,
+// so that consecutive tiles (contiguous memory) run on one XCD (workgroups are
+// dispatched to the 8 XCDs round-robin).
+#ifndef PAT_XCD_SWIZZLE
+#define PAT_XCD_SWIZZLE 0
 #endif
 
 namespace pat {
@@ -58,17 +65,17 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // through an explicit global (address space 1) pointer instead.
 #define PAT_GLOBAL __attribute__((address_space(1)))
 
-template <typename T>
+template <typename T, bool NT>
 __device__ __forceinline__ T ldg(const char* p) {
   const PAT_GLOBAL T* q = (const PAT_GLOBAL T*)(p);
-  if constexpr (PAT_NONTEMPORAL) return __builtin_nontemporal_load(q);
+  if constexpr (NT) return __builtin_nontemporal_load(q);
   return *q;
 }
 
 template <typename T>
 __device__ __forceinline__ void stg(char* p, const T& v) {
   PAT_GLOBAL T* q = (PAT_GLOBAL T*)(p);
-  if constexpr (PAT_NONTEMPORAL)
+  if constexpr (PAT_NT_STORES)
     __builtin_nontemporal_store(v, q);
   else
     *q = v;
@@ -105,7 +112,7 @@ __device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r,
 // All-gather
 // ---------------------------------------------------------------------------
 
-template <typename Unit, int U>
+template <typename Unit, int U, bool NTL>
 struct AgOp {
   static constexpr int kTile = kThreads * U;
 
@@ -150,7 +157,7 @@ struct AgOp {
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t v = v0 + j * kThreads;
-        if (v < st.V) x[j] = ldg<Unit>(e.src + v * (int64_t)sizeof(Unit));
+        if (v < st.V) x[j] = ldg<Unit, NTL>(e.src + v * (int64_t)sizeof(Unit));
       }
 #pragma unroll
       for (int j = 0; j < U; ++j) {
@@ -170,7 +177,7 @@ struct AgOp {
           int r, i;
           split_flat(g, st, &r, &i, &vv[j], small);
           e[j] = edge(cx, st, r, i);
-          x[j] = ldg<Unit>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+          x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
         }
       }
 #pragma unroll
@@ -264,7 +271,7 @@ struct TB16S {
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
 };
 
-template <class R>
+template <class R, bool NTL>
 struct RsOp {
   using in_t = typename R::in_t;
   using acc_t = typename R::acc_t;
@@ -306,8 +313,8 @@ struct RsOp {
   }
 
   __device__ static acc_t load(const char* p, bool raw, int64_t v) {
-    if (raw) return R::widen(ldg<in_t>(p + v * (int64_t)sizeof(in_t)));
-    return ldg<acc_t>(p + v * (int64_t)sizeof(acc_t));
+    if (raw) return R::widen(ldg<in_t, NTL>(p + v * (int64_t)sizeof(in_t)));
+    return ldg<acc_t, NTL>(p + v * (int64_t)sizeof(acc_t));
   }
 
   __device__ static void store(const Edge& e, int64_t v, const acc_t& x) {
@@ -370,6 +377,13 @@ struct RsOp {
 template <class Op>
 __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, int s) {
   const DevStep st = cx.steps[s];
+  if (PAT_XCD_SWIZZLE) {
+    // grid = 8 * ceil(items / 8) (no grid-stride): see launch_step_t
+    const int64_t q = (st.items + 7) / 8;
+    const int64_t item = (int64_t)(blockIdx.x % 8) * q + blockIdx.x / 8;
+    if (item < st.items) Op::run(cx, st, item);
+    return;
+  }
   for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
 }
 
@@ -431,7 +445,11 @@ template <class Op>
 hipError_t launch_step_t(const KCtx& cx, int s, int64_t items, hipStream_t stream) {
   if (items <= 0) return hipSuccess;
   const int64_t cap = int64_t(1) << 30;
-  const unsigned grid = (unsigned)(items < cap ? items : cap);
+  unsigned grid = (unsigned)(items < cap ? items : cap);
+  if (PAT_XCD_SWIZZLE) {
+    if (items > cap) return hipErrorInvalidValue;
+    grid = (unsigned)((items + 7) / 8 * 8);
+  }
   hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, s);
   return hipGetLastError();
 }
@@ -457,22 +475,18 @@ hipError_t capacity_t(int* blocks) {
   return hipSuccess;
 }
 
-using AgV = AgOp<v4u, PAT_UNROLL>;
-using Ag4 = AgOp<uint32_t, 4>;
-using Ag2 = AgOp<uint16_t, 4>;
-
-#define PAT_DISPATCH(v, CALL)                    \
-  switch (v) {                                   \
-    case kAgVec: return CALL(AgV);               \
-    case kAgS4: return CALL(Ag4);                \
-    case kAgS2: return CALL(Ag2);                \
-    case kRsI32Vec: return CALL(RsOp<TI32V>);    \
-    case kRsF32Vec: return CALL(RsOp<TF32V>);    \
-    case kRsB16Vec: return CALL(RsOp<TB16V>);    \
-    case kRsI32S: return CALL(RsOp<TI32S>);      \
-    case kRsF32S: return CALL(RsOp<TF32S>);      \
-    case kRsB16S: return CALL(RsOp<TB16S>);      \
-    default: return hipErrorInvalidValue;        \
+#define PAT_DISPATCH(v, NT, CALL)                                           \
+  switch (v) {                                                              \
+    case kAgVec: return NT ? CALL((AgOp<v4u, PAT_UNROLL, true>)) : CALL((AgOp<v4u, PAT_UNROLL, false>)); \
+    case kAgS4: return NT ? CALL((AgOp<uint32_t, 4, true>)) : CALL((AgOp<uint32_t, 4, false>));         \
+    case kAgS2: return NT ? CALL((AgOp<uint16_t, 4, true>)) : CALL((AgOp<uint16_t, 4, false>));         \
+    case kRsI32Vec: return NT ? CALL((RsOp<TI32V, true>)) : CALL((RsOp<TI32V, false>));                  \
+    case kRsF32Vec: return NT ? CALL((RsOp<TF32V, true>)) : CALL((RsOp<TF32V, false>));                  \
+    case kRsB16Vec: return NT ? CALL((RsOp<TB16V, true>)) : CALL((RsOp<TB16V, false>));                  \
+    case kRsI32S: return NT ? CALL((RsOp<TI32S, true>)) : CALL((RsOp<TI32S, false>));                    \
+    case kRsF32S: return NT ? CALL((RsOp<TF32S, true>)) : CALL((RsOp<TF32S, false>));                    \
+    case kRsB16S: return NT ? CALL((RsOp<TB16S, true>)) : CALL((RsOp<TB16S, false>));                    \
+    default: return hipErrorInvalidValue;                                   \
   }
 
 }  // namespace
@@ -494,34 +508,36 @@ int variant_in_bytes(Variant v) {
 
 int variant_tile(Variant v) {
   switch (v) {
-    case kAgVec: return AgV::kTile;
-    case kAgS4: return Ag4::kTile;
-    case kAgS2: return Ag2::kTile;
-    case kRsI32Vec: return RsOp<TI32V>::kTile;
-    case kRsF32Vec: return RsOp<TF32V>::kTile;
-    case kRsB16Vec: return RsOp<TB16V>::kTile;
-    case kRsI32S: return RsOp<TI32S>::kTile;
-    case kRsF32S: return RsOp<TF32S>::kTile;
-    case kRsB16S: return RsOp<TB16S>::kTile;
+    case kAgVec: return AgOp<v4u, PAT_UNROLL, true>::kTile;
+    case kAgS4: return AgOp<uint32_t, 4, true>::kTile;
+    case kAgS2: return AgOp<uint16_t, 4, true>::kTile;
+    case kRsI32Vec: return RsOp<TI32V, true>::kTile;
+    case kRsF32Vec: return RsOp<TF32V, true>::kTile;
+    case kRsB16Vec: return RsOp<TB16V, true>::kTile;
+    case kRsI32S: return RsOp<TI32S, true>::kTile;
+    case kRsF32S: return RsOp<TF32S, true>::kTile;
+    case kRsB16S: return RsOp<TB16S, true>::kTile;
     default: return 0;
   }
 }
 
-hipError_t launch_step(Variant v, const KCtx& cx, int s, int64_t items, hipStream_t stream) {
-#define PAT_STEP(OP) launch_step_t<OP>(cx, s, items, stream)
-  PAT_DISPATCH(v, PAT_STEP)
+#define PAT_UNPAREN(...) __VA_ARGS__
+
+hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, int s, int64_t items, hipStream_t stream) {
+#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, s, items, stream)
+  PAT_DISPATCH(v, nt_loads, PAT_STEP)
 #undef PAT_STEP
 }
 
-hipError_t launch_persistent(Variant v, const KCtx& cx, int grid, hipStream_t stream) {
-#define PAT_PERS(OP) launch_persistent_t<OP>(cx, grid, stream)
-  PAT_DISPATCH(v, PAT_PERS)
+hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream) {
+#define PAT_PERS(OP) launch_persistent_t<PAT_UNPAREN OP>(cx, grid, stream)
+  PAT_DISPATCH(v, nt_loads, PAT_PERS)
 #undef PAT_PERS
 }
 
-hipError_t persistent_capacity(Variant v, int* blocks) {
-#define PAT_CAP(OP) capacity_t<OP>(blocks)
-  PAT_DISPATCH(v, PAT_CAP)
+hipError_t persistent_capacity(Variant v, bool nt_loads, int* blocks) {
+#define PAT_CAP(OP) capacity_t<PAT_UNPAREN OP>(blocks)
+  PAT_DISPATCH(v, nt_loads, PAT_CAP)
 #undef PAT_CAP
 }
 
