@@ -380,8 +380,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
                      capacity, plan->cus, grid, cx.nsteps);
     HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
   } else if (mode == PAT_EXEC_STREAM) {
-    for (size_t s = 0; s < steps.size(); ++s)
-      HIP_TRY(pat::launch_step(var, plan->nt_loads, cx, (int)s, steps[s].items, stream));
+    for (size_t s = 0; s < steps.size(); ++s) HIP_TRY(pat::launch_step(var, plan->nt_loads, cx, steps[s], stream));
   } else {
     hipGraphExec_t& exec = plan->graph[vi][cx.own_copy];
     if (!exec) {
@@ -390,7 +389,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
       hipGraph_t g = nullptr;
       hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
       for (size_t s = 0; e == hipSuccess && s < steps.size(); ++s)
-        e = pat::launch_step(var, plan->nt_loads, cx, (int)s, steps[s].items, cs);
+        e = pat::launch_step(var, plan->nt_loads, cx, steps[s], cs);
       const hipError_t e2 = hipStreamEndCapture(cs, &g);
       if (e == hipSuccess) e = e2;
       if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);

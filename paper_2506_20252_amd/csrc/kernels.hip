@@ -108,6 +108,14 @@ __device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r,
   }
 }
 
+// Split a tiled work item into (rank, entry, tile).
+__device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int* r, int* i, int64_t* tile) {
+  const int64_t e = item / st.tiles_per_edge;
+  *tile = item - e * st.tiles_per_edge;
+  *r = (int)(e / st.k);
+  *i = (int)(e - (int64_t)(*r) * st.k);
+}
+
 // ---------------------------------------------------------------------------
 // All-gather
 // ---------------------------------------------------------------------------
@@ -148,10 +156,9 @@ struct AgOp {
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
     Unit x[U];
     if (st.tiles_per_edge > 0) {
-      const int64_t eid = item / st.tiles_per_edge;
-      const int64_t tile = item - eid * st.tiles_per_edge;
-      const int r = (int)(eid / st.k);
-      const int i = (int)(eid - (int64_t)r * st.k);
+      int r, i;
+      int64_t tile;
+      split_tile(item, st, &r, &i, &tile);
       const Edge e = edge(cx, st, r, i);
       const int64_t v0 = tile * kTile + threadIdx.x;
 #pragma unroll
@@ -327,10 +334,9 @@ struct RsOp {
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
     acc_t a[U], b[U];
     if (st.tiles_per_edge > 0) {
-      const int64_t eid = item / st.tiles_per_edge;
-      const int64_t tile = item - eid * st.tiles_per_edge;
-      const int r = (int)(eid / st.k);
-      const int i = (int)(eid - (int64_t)r * st.k);
+      int r, i;
+      int64_t tile;
+      split_tile(item, st, &r, &i, &tile);
       const Edge e = edge(cx, st, r, i);
       const int64_t v0 = tile * kTile + threadIdx.x;
 #pragma unroll
@@ -374,9 +380,9 @@ struct RsOp {
 // Drivers
 // ---------------------------------------------------------------------------
 
+// One launch per step; the step descriptor comes by value with the launch.
 template <class Op>
-__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, int s) {
-  const DevStep st = cx.steps[s];
+__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
   if (PAT_XCD_SWIZZLE) {
     // grid = 8 * ceil(items / 8) (no grid-stride): see launch_step_t
     const int64_t q = (st.items + 7) / 8;
@@ -442,7 +448,8 @@ __global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
 }
 
 template <class Op>
-hipError_t launch_step_t(const KCtx& cx, int s, int64_t items, hipStream_t stream) {
+hipError_t launch_step_t(const KCtx& cx, const DevStep& st, hipStream_t stream) {
+  const int64_t items = st.items;
   if (items <= 0) return hipSuccess;
   const int64_t cap = int64_t(1) << 30;
   unsigned grid = (unsigned)(items < cap ? items : cap);
@@ -450,7 +457,7 @@ hipError_t launch_step_t(const KCtx& cx, int s, int64_t items, hipStream_t strea
     if (items > cap) return hipErrorInvalidValue;
     grid = (unsigned)((items + 7) / 8 * 8);
   }
-  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, s);
+  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, st);
   return hipGetLastError();
 }
 
@@ -523,8 +530,8 @@ int variant_tile(Variant v) {
 
 #define PAT_UNPAREN(...) __VA_ARGS__
 
-hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, int s, int64_t items, hipStream_t stream) {
-#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, s, items, stream)
+hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream) {
+#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, stream)
   PAT_DISPATCH(v, nt_loads, PAT_STEP)
 #undef PAT_STEP
 }

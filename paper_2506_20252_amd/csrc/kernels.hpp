@@ -55,7 +55,7 @@ int variant_tile(Variant v);
 
 // nt_loads: nontemporal (streaming) loads, for operations much larger than the
 // 256 MB Infinity Cache; plain loads let small operations hit in it.
-hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, int s, int64_t items, hipStream_t stream);
+hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream);
 hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream);
 // Workgroups of the persistent kernel that fit on the current device at once.
 hipError_t persistent_capacity(Variant v, bool nt_loads, int* blocks);

@@ -173,7 +173,7 @@ def test_workload2_ag_bf16_n24():
     np.testing.assert_array_equal(got, D.allgather(host_in))
 
 
-@pytest.mark.parametrize("mode", ["persistent", "graph"])
+@pytest.mark.parametrize("mode", ["persistent", "graph", "stream"])
 def test_workload3_rs_f32_n64(mode):
     n, count, seed = 64, 262144, 0x5041543
     rng = np.random.default_rng(3)
@@ -201,12 +201,13 @@ def test_workload4_small_chunks_n1000():
     assert (np.abs(got.astype(np.float64) - exact) <= 1e-5 * scale).all()
 
 
-def test_workload5_rs_bf16_n128_full_size():
+@pytest.mark.parametrize("mode", ["stream", "graph"])
+def test_workload5_rs_bf16_n128_full_size(mode):
     n, count, seed = 128, 2 * MIB, 0x5041545
     rng = np.random.default_rng(5)
     sample = np.unique(np.concatenate([[0, 1, 7, 8, 2047, 2048, count - 8, count - 1],
                                        rng.integers(0, count, 1500)]))
-    got = run_rs(n, count, "bfloat16", seed, sample=sample)
+    got = run_rs(n, count, "bfloat16", seed, sample=sample, mode=mode)
     torch.cuda.empty_cache()
     host_in = host_rs_inputs(n, count, "bf16_normal", seed, sample)
     check_rs(got, host_in, "bfloat16", oracle_t(pat.PAT_REDUCESCATTER, n, count, "bfloat16"))
@@ -221,14 +222,15 @@ def test_workload5_rs_bf16_n128_full_size():
 SWEEP_N = [2, 3, 5, 7, 8, 13, 16, 33]
 
 
+@pytest.mark.parametrize("mode", ["stream", "graph"])
 @pytest.mark.parametrize("n", SWEEP_N)
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 @pytest.mark.parametrize("count", [1, 17, 1000, 4104])
-def test_sweep_default_budget(n, dtype, count):
+def test_sweep_default_budget(n, dtype, count, mode):
     seed = 1000 * n + count
-    got, host_in = run_ag(n, count, dtype, seed)
+    got, host_in = run_ag(n, count, dtype, seed, mode=mode)
     np.testing.assert_array_equal(got, D.allgather(host_in))
-    got = run_rs(n, count, dtype, seed + 1)
+    got = run_rs(n, count, dtype, seed + 1, mode=mode)
     check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
              oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
 
@@ -251,39 +253,42 @@ def test_sweep_budgets_and_modes(n, budget, mode):
         pat.check(pat.pat_set_buffer_bytes(0))
 
 
+@pytest.mark.parametrize("mode", ["stream", "graph"])
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 @pytest.mark.parametrize("n", [1, 6, 9])
-def test_in_place(n, dtype):
+def test_in_place(n, dtype, mode):
     count = 1000
-    got, host_in = run_ag(n, count, dtype, 77 + n, inplace=True)
+    got, host_in = run_ag(n, count, dtype, 77 + n, inplace=True, mode=mode)
     np.testing.assert_array_equal(got, D.allgather(host_in))
-    got = run_rs(n, count, dtype, 78 + n, inplace=True)
+    got = run_rs(n, count, dtype, 78 + n, inplace=True, mode=mode)
     check_rs(got, host_rs_inputs(n, count, DIST[dtype], 78 + n), dtype,
              oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
 
 
 def test_repeated_calls_reuse_plan_and_tables():
     """Same plan, different buffers on the second call (pointer tables re-uploaded)."""
+    modes = ["persistent", "graph", "stream"]
     for rep in range(3):
-        got, host_in = run_ag(12, 256, "float32", 500 + rep, mode=["persistent", "graph", "stream"][rep])
+        got, host_in = run_ag(12, 256, "float32", 500 + rep, mode=modes[rep])
         np.testing.assert_array_equal(got, D.allgather(host_in))
-        got = run_rs(12, 256, "float32", 600 + rep, mode=["persistent", "graph", "stream"][rep])
+        got = run_rs(12, 256, "float32", 600 + rep, mode=modes[rep])
         check_rs(got, host_rs_inputs(12, 256, "f32_normal", 600 + rep), "float32",
                  oracle_t(pat.PAT_REDUCESCATTER, 12, 256, "float32"))
 
 
+@pytest.mark.parametrize("mode", ["stream", "graph"])
 @pytest.mark.parametrize("n", [6, 13, 33])
 @pytest.mark.parametrize("budget", [4096, 65536])
-def test_close_first_linear_order(n, budget):
+def test_close_first_linear_order(n, budget, mode):
     count = 4104
     pat.check(pat.pat_set_buffer_bytes(budget))
     pat.check(pat.pat_set_linear_order("close"))
     try:
         for dtype in ("float32", "bfloat16", "int32"):
             seed = 31 * n + budget
-            got, host_in = run_ag(n, count, dtype, seed)
+            got, host_in = run_ag(n, count, dtype, seed, mode=mode)
             np.testing.assert_array_equal(got, D.allgather(host_in))
-            got = run_rs(n, count, dtype, seed + 1)
+            got = run_rs(n, count, dtype, seed + 1, mode=mode)
             host = host_rs_inputs(n, count, DIST[dtype], seed + 1)
             if dtype == "int32":
                 np.testing.assert_array_equal(got, D.reducescatter_sum(host, "int32"))
