@@ -393,17 +393,22 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
   for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
 }
 
-// Device-wide barrier for the persistent kernel.  Every thread fences its
-// writes at agent scope (write-back of this XCD's L2), one thread per block
-// counts in and polls until every block has arrived or the wall-clock limit
-// passes, and every thread fences again before reading what other blocks
-// wrote.  Returns false if the wait gave up (status bit set); the block then
-// stops.
+// Device-wide barrier for the persistent kernel.
+//  1. Every wave waits until its own stores are complete (acknowledged by this
+//     XCD's L2): a workgroup barrier alone does not wait for them.
+//  2. After the workgroup barrier, one thread counts in with an agent-scope
+//     release (one write-back of the XCD's L2, whose lines now include every
+//     wave's stores), then polls until all workgroups have arrived or the
+//     wall-clock limit passes, and takes an agent-scope acquire (invalidates
+//     this CU's L1 and the L2 lines other XCDs may have changed).
+//  3. A second workgroup barrier releases the other waves, whose loads come
+//     after the invalidation.
+// Returns false if the wait gave up (status bit set); the block then stops.
 __device__ bool grid_barrier(const KCtx& cx, unsigned target, int* s_ok) {
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(&cx.bar[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(&cx.bar[0], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     const long long t0 = wall_clock64();
     int ok = 1;
     while ((int)(__hip_atomic_load(&cx.bar[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
@@ -414,10 +419,10 @@ __device__ bool grid_barrier(const KCtx& cx, unsigned target, int* s_ok) {
         break;
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     *s_ok = ok;
   }
   __syncthreads();
-  __threadfence();
   return *s_ok != 0;
 }
 

@@ -326,3 +326,29 @@ def test_persistent_barrier_timeout_is_reported_and_recovers():
     got = run_rs(n, count, "float32", seed, mode="persistent", sample=sample)
     check_rs(got, host_rs_inputs(n, count, "f32_normal", seed, sample), "float32",
              oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
+
+
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+def test_back_to_back_calls_with_new_buffers_no_host_sync(mode):
+    """Three operations on one plan, each with its own buffers, queued without
+    any host synchronisation: the pointer tables are re-staged each call while
+    the previous call may still be running."""
+    n, count = 11, 2048
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode(mode))
+    stream = torch.cuda.current_stream()
+    sends, recvs = [], []
+    for rep in range(3):
+        send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+        fill_ranks(send, "f32_normal", 900 + rep)
+        recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+        sends.append(send)
+        recvs.append(recv)
+    log(f"[gpu] three queued reduce-scatters, mode={mode}")
+    for rep in range(3):
+        pat.check(pat.pat_reducescatter(list(sends[rep]), list(recvs[rep]), count, "float32", pat.PAT_SUM, n,
+                                        stream))
+    pat.check(pat.pat_check_device_status(stream))
+    for rep in range(3):
+        check_rs(as_bits(recvs[rep]), host_rs_inputs(n, count, "f32_normal", 900 + rep), "float32",
+                 oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
