@@ -165,6 +165,58 @@ def small_size_latency(reps=200):
     return out
 
 
+def other_workloads(reps=50):
+    """Workloads 1-3 timed the same way (HIP events around back-to-back
+    operations): microseconds per operation, aggregate bus bandwidth and the
+    fraction of HBM peak that the algorithmic bytes reach."""
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    tdt = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}
+    rows = []
+    for wid in (1, 2, 3):
+        coll, n, count, dtype, dist, seed, desc = WORKLOADS[wid]
+        if coll == "rs":
+            send = torch.empty((n, n * count), dtype=tdt[dtype], device=dev)
+            recv = torch.empty((n, count), dtype=tdt[dtype], device=dev)
+            code = pat.PAT_REDUCESCATTER
+        else:
+            send = torch.empty((n, count), dtype=tdt[dtype], device=dev)
+            recv = torch.empty((n, n * count), dtype=tdt[dtype], device=dev)
+            code = pat.PAT_ALLGATHER
+        for x in range(n):
+            synth.fill(send[x], dist, seed, x)
+        S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+
+        def op():
+            if coll == "rs":
+                return pat.pat_reducescatter(S, R, count, dtype, pat.PAT_SUM, n, stream)
+            return pat.pat_allgather(S, R, count, dtype, n, stream)
+
+        for _ in range(5):
+            pat.check(op())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            pat.check(op())
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pat.check(pat.pat_check_device_status(stream))
+        sec = e0.elapsed_time(e1) / 1e3 / reps
+        st, info = pat.pat_plan_info(code, n, count, dtype)
+        rows.append({"workload": desc, "us": round(sec * 1e6, 2), "steps": info["steps"],
+                     "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
+                     "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
+        del send, recv, S, R
+    torch.cuda.empty_cache()
+    return rows
+
+
 def copy_probe(nbytes, reps):
     """A plain device-to-device copy of known size: reads and writes nbytes."""
     import torch
@@ -297,6 +349,7 @@ def main():
     }
     if not args.no_latency:
         out["small_size_latency"] = small_size_latency()
+        out["other_workloads"] = other_workloads()
     if not args.no_cpu_baseline:
         # The oracle's inputs: the first m positions of every chunk of the
         # generator-filled send buffers (the collective only reads them).

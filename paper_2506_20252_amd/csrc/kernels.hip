@@ -6,10 +6,13 @@
 //           addresses computed once per workgroup (wavefront-uniform);
 //   packed: chunks smaller than a tile; consecutive vectors of consecutive
 //           edges, addresses computed per lane.
-// Every lane issues all of its loads before any store (kUnroll vectors of
-// 16 bytes in flight per stream).  The data path has no matrix work and no
-// reuse, so there is no LDS staging: a 128-bit load lands in VGPRs and is
-// stored from there.
+// Every lane issues all of its loads before any store: kUnroll vectors per
+// stream, 16 bytes each (bf16 reduce-scatter: 8-byte inputs beside 16-byte
+// float32 partials, at twice the unroll).  Accesses use explicit global
+// pointers, stores are nontemporal, and loads are nontemporal for operations
+// far larger than the Infinity Cache.  The data path has no matrix work and no
+// reuse, so there is no LDS staging: a load lands in VGPRs and is stored from
+// there.
 //
 // All-gather step (section "The PAT algorithm"): the sender at tree position
 // p copies chunk (r - p) mod N from its send buffer (p = 0) or from the slot
