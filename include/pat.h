@@ -193,6 +193,15 @@ pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat
                             int32_t* a, int32_t* b, int32_t* c, int max_entries, int* nsteps,
                             int* nentries);
 
+/* Cached plans: their number and the device memory they hold, all devices.
+ * Plans are cached per (operation, nranks, count, dtype, budget, linear
+ * order, device).  When a new plan would take a device's cached plans past
+ * PAT_PLAN_CACHE_BYTES (default 32 GiB), the least recently used plans of that
+ * device are released first, each after its last operation has finished on
+ * its stream; an allocation failure releases every other plan of the device
+ * and retries once.  Host-only. */
+pat_status_t pat_cache_stats(int* plans, size_t* bytes);
+
 /* Waits for `stream`, then reports (and clears) a barrier timeout recorded by
  * a persistent kernel on the current device: PAT_OK or PAT_ERR_TIMEOUT. */
 pat_status_t pat_check_device_status(hipStream_t stream);

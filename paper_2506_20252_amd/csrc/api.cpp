@@ -112,11 +112,16 @@ struct Plan {
   bool nt_loads = true;
   int cus = 0;
   int64_t clock_khz = 0;
+  size_t bytes = 0;          // device memory held (slots, accumulators, tables)
+  hipEvent_t done = nullptr;  // recorded after the plan's last operation
+  bool used = false;
+  uint64_t last_use = 0;     // LRU stamp
 
   ~Plan() {
     for (auto& row : graph)
       for (auto& g : row)
         if (g) (void)hipGraphExecDestroy(g);
+    if (done) (void)hipEventDestroy(done);
     if (upload_done) (void)hipEventDestroy(upload_done);
     if (pinned) (void)hipHostFree(pinned);
     (void)hipFree(d_entries);
@@ -132,6 +137,37 @@ struct Plan {
 
 using PlanKey = std::tuple<int, int, int64_t, int, size_t, int, int>;  // coll, N, count, dtype, budget, order, device
 std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
+uint64_t g_tick = 0;
+
+// Device memory the cached plans of one device may hold before the least
+// recently used ones are released (PAT_PLAN_CACHE_BYTES; default 32 GiB).  A
+// single plan larger than this is still allowed.
+size_t cache_cap() {
+  if (const char* e = std::getenv("PAT_PLAN_CACHE_BYTES")) {
+    const long long v = std::atoll(e);
+    if (v > 0) return size_t(v);
+  }
+  return size_t(32) << 30;
+}
+
+// Release least recently used plans of `device` until `need` more bytes fit
+// under the cap (need == SIZE_MAX: release them all).  A plan's buffers are
+// freed only after its last operation has finished on its stream.
+void make_room(int device, size_t need) {
+  for (;;) {
+    size_t held = 0;
+    auto victim = g_plans.end();
+    for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
+      if (it->second->device != device) continue;
+      held += it->second->bytes;
+      if (victim == g_plans.end() || it->second->last_use < victim->second->last_use) victim = it;
+    }
+    if (victim == g_plans.end()) return;
+    if (need != SIZE_MAX && held + need <= cache_cap()) return;
+    if (victim->second->used) (void)hipEventSynchronize(victim->second->done);
+    g_plans.erase(victim);
+  }
+}
 
 // Launch-level steps for one vector width: every schedule step of every piece.
 bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, std::vector<pat::DevStep>* out) {
@@ -189,10 +225,20 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
   if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)round_up(size_t(d.piece_elems) * 4, 256);
+  p->bytes = size_t(p->slot_rank_stride + p->rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
+             (p->steps[0].size() + p->steps[1].size()) * sizeof(pat::DevStep) + 2 * N * sizeof(void*) + 16;
+  make_room(device, p->bytes);
 
-  auto alloc = [](void** ptr, size_t bytes) -> pat_status_t {
+  // On an allocation failure, release every other cached plan of this device
+  // and try once more.
+  auto alloc = [device](void** ptr, size_t bytes) -> pat_status_t {
     if (bytes == 0) return PAT_OK;
     hipError_t e = hipMalloc(ptr, bytes);
+    if (e == hipErrorOutOfMemory) {
+      (void)hipGetLastError();
+      make_room(device, SIZE_MAX);
+      e = hipMalloc(ptr, bytes);
+    }
     if (e == hipErrorOutOfMemory) {
       (void)hipGetLastError();
       return PAT_ERR_OUT_OF_MEMORY;
@@ -228,6 +274,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
                         hipMemcpyHostToDevice));
   HIP_TRY(hipHostMalloc((void**)&p->pinned, 2 * size_t(N) * sizeof(void*), hipHostMallocDefault));
   HIP_TRY(hipEventCreateWithFlags(&p->upload_done, hipEventDisableTiming));
+  HIP_TRY(hipEventCreateWithFlags(&p->done, hipEventDisableTiming));
   if (const char* e = std::getenv("PAT_DEBUG")) {
     if (e[0] == '1') {
       std::fprintf(stderr,
@@ -403,6 +450,9 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     }
     HIP_TRY(hipGraphLaunch(exec, stream));
   }
+  HIP_TRY(hipEventRecord(plan->done, stream));
+  plan->used = true;
+  plan->last_use = ++g_tick;
   return PAT_OK;
 }
 
@@ -528,6 +578,16 @@ pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat
     if (b) b[j] = d.entries[j].b;
     if (c) c[j] = d.entries[j].c;
   }
+  return PAT_OK;
+}
+
+pat_status_t pat_cache_stats(int* plans, size_t* bytes) {
+  if (!plans || !bytes) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  *plans = (int)g_plans.size();
+  size_t b = 0;
+  for (const auto& kv : g_plans) b += kv.second->bytes;
+  *bytes = b;
   return PAT_OK;
 }
 

@@ -49,7 +49,7 @@ EXPORTS = (
     "pat_allgather", "pat_reducescatter", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
     "pat_set_barrier_timeout_us", "pat_plan_info",
-    "pat_plan_steps", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
+    "pat_plan_steps", "pat_cache_stats", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
     "pat_finalize",
 )
 
@@ -103,6 +103,7 @@ def lib():
             "pat_plan_steps": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, _I32P, _I32P,
                                 ctypes.c_int, _I32P, _I32P, _I32P, _I32P, ctypes.c_int,
                                 ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
+            "pat_cache_stats": ([ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "pat_check_device_status": ([_P], ctypes.c_int),
             "pat_last_hip_error": ([], ctypes.c_int),
             "pat_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -209,6 +210,13 @@ def pat_plan_steps(coll, nranks, count, dtype):
     steps = [(d[i], k[i]) for i in range(ns.value)]
     entries = [(pos[j], a[j], b[j], c[j]) for j in range(ne.value)]
     return st, steps, entries
+
+
+def pat_cache_stats():
+    """Returns (status, number of cached plans, device bytes they hold)."""
+    n, b = ctypes.c_int(), ctypes.c_size_t()
+    st = lib().pat_cache_stats(ctypes.byref(n), ctypes.byref(b))
+    return st, n.value, b.value
 
 
 def pat_check_device_status(stream=None):

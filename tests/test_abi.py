@@ -78,6 +78,7 @@ def test_settings_roundtrip():
     assert pat.pat_set_buffer_bytes(1 << 20) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 1 << 20
     assert pat.pat_set_buffer_bytes(0) == pat.PAT_OK and pat.pat_get_buffer_bytes() == 8 << 20
     assert pat.pat_finalize() == pat.PAT_OK  # nothing allocated: no device call
+    assert pat.pat_cache_stats() == (pat.PAT_OK, 0, 0)
 
 
 def test_plan_info_workloads():

@@ -352,3 +352,20 @@ def test_back_to_back_calls_with_new_buffers_no_host_sync(mode):
     for rep in range(3):
         check_rs(as_bits(recvs[rep]), host_rs_inputs(n, count, "f32_normal", 900 + rep), "float32",
                  oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
+
+
+def test_plan_cache_is_bounded_and_evicts_safely():
+    """With a 1-byte cap every new plan releases the previous one, after its
+    last operation; results stay exact, and an evicted shape is rebuilt."""
+    os.environ["PAT_PLAN_CACHE_BYTES"] = "1"
+    try:
+        pat.check(pat.pat_finalize())
+        for i, count in enumerate([4096, 8192, 16384, 4096]):
+            got = run_rs(16, count, "float32", 1234 + i)
+            st, plans, nbytes = pat.pat_cache_stats()
+            assert st == pat.PAT_OK and plans == 1 and nbytes > 0
+            check_rs(got, host_rs_inputs(16, count, "f32_normal", 1234 + i), "float32",
+                     oracle_t(pat.PAT_REDUCESCATTER, 16, count, "float32"))
+    finally:
+        os.environ.pop("PAT_PLAN_CACHE_BYTES", None)
+        pat.check(pat.pat_finalize())
