@@ -22,6 +22,7 @@ python bench.py [--steps K] [--warmup W] [--mode persistent|graph|stream]
 
 import argparse
 import hashlib
+import math
 import json
 import os
 import re
@@ -217,6 +218,69 @@ def other_workloads(reps=50):
     return rows
 
 
+def budget_sweep(wid, reps):
+    """Time one workload at every aggregation level: the budget is set to the
+    bytes of the largest step at T = 1, 2, 4, ... up to full aggregation, so
+    the plan goes from one linear tree (N - 1 steps) to ceil(log2 N) steps."""
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    coll, n, count, dtype, dist, seed, desc = WORKLOADS[wid]
+    tdt = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}[dtype]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    if coll == "rs":
+        send = torch.empty((n, n * count), dtype=tdt, device=dev)
+        recv = torch.empty((n, count), dtype=tdt, device=dev)
+        code = pat.PAT_REDUCESCATTER
+    else:
+        send = torch.empty((n, count), dtype=tdt, device=dev)
+        recv = torch.empty((n, n * count), dtype=tdt, device=dev)
+        code = pat.PAT_ALLGATHER
+    for x in range(n):
+        synth.fill(send[x], dist, seed, x)
+    S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+    slot_elem = 4 if (coll == "rs" or dtype != "bfloat16") else (2 if dtype == "bfloat16" else 4)
+    rows = []
+    T = 1
+    while True:
+        budget = T * count * slot_elem
+        pat.check(pat.pat_set_buffer_bytes(budget))
+        st, info = pat.pat_plan_info(code, n, count, dtype)
+        if info["T"] < T:
+            break
+
+        def op():
+            if coll == "rs":
+                return pat.pat_reducescatter(S, R, count, dtype, pat.PAT_SUM, n, stream)
+            return pat.pat_allgather(S, R, count, dtype, n, stream)
+
+        for _ in range(3):
+            pat.check(op())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            pat.check(op())
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pat.check(pat.pat_check_device_status(stream))
+        sec = e0.elapsed_time(e1) / 1e3 / reps
+        rows.append({"budget_bytes": budget, "T": info["T"], "steps": info["steps"],
+                     "slot_bytes_per_rank": info["slot_bytes_per_rank"], "us": round(sec * 1e6, 2),
+                     "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
+                     "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
+        pat.check(pat.pat_finalize())
+        if info["T"] * 2 > (1 << max(info["L"] - 1, 0)):
+            break
+        T *= 2
+    pat.check(pat.pat_set_buffer_bytes(0))
+    print(json.dumps({"metric": "PAT budget sweep (steps and time per aggregation level)", "workload": desc,
+                      "nranks": n, "log2_n": round(math.log2(n), 3), "rows": rows}), flush=True)
+
+
 def copy_probe(nbytes, reps):
     """A plain device-to-device copy of known size: reads and writes nbytes."""
     import torch
@@ -249,6 +313,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true", help="skip the small-size latency figures")
+    ap.add_argument("--budget-sweep", action="store_true",
+                    help="instead: time the workload at every aggregation level (T = 1 .. full)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: all virtual ranks are emulated on one GPU; runs on more than one GPU "
@@ -259,6 +325,9 @@ def main():
 
     if args.copy_probe:
         copy_probe(args.copy_probe, args.steps)
+        return
+    if args.budget_sweep:
+        budget_sweep(args.workload, args.steps)
         return
 
     import synth
