@@ -218,10 +218,11 @@ def other_workloads(reps=50):
     return rows
 
 
-def budget_sweep(wid, reps):
+def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
     """Time one workload at every aggregation level: the budget is set to the
     bytes of the largest step at T = 1, 2, 4, ... up to full aggregation, so
-    the plan goes from one linear tree (N - 1 steps) to ceil(log2 N) steps."""
+    the plan goes from one linear tree (N - 1 steps) to ceil(log2 N) steps,
+    stopping early once the slots of all ranks would exceed max_slot_bytes."""
     import torch
 
     import synth
@@ -249,7 +250,7 @@ def budget_sweep(wid, reps):
         budget = T * count * slot_elem
         pat.check(pat.pat_set_buffer_bytes(budget))
         st, info = pat.pat_plan_info(code, n, count, dtype)
-        if info["T"] < T:
+        if info["T"] < T or info["slot_bytes_total"] > max_slot_bytes:
             break
 
         def op():
