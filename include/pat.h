@@ -75,9 +75,13 @@ typedef enum {
 } pat_collective_t;
 
 typedef enum {
-  /* One cooperative launch per operation; a device-wide barrier separates
-   * the steps.  Its grid is capped at 2 workgroups per compute unit
-   * (PAT_PERSISTENT_BLOCKS_PER_CU overrides) so that it is co-resident. */
+  /* One launch per operation.  Workgroups take per-step work from device
+   * counters in step order, and step s starts only when every piece of step
+   * s - 1 is done.  It needs no co-residency, so any grid size is safe; the
+   * grid is 2, 4 or all workgroups per compute unit by bytes per step
+   * (PAT_PERSISTENT_BLOCKS_PER_CU overrides).  Each step costs a few
+   * microseconds of device-scope synchronisation, more than a kernel
+   * boundary, so the stream mode is faster on MI355X. */
   PAT_EXEC_PERSISTENT = 0,
   /* One kernel per step, captured once per plan (and vector width) into a
    * HIP graph and replayed. */
@@ -143,8 +147,8 @@ int pat_get_linear_order(void);
 pat_status_t pat_set_exec_mode(int mode);
 int pat_get_exec_mode(void);
 
-/* Wall-clock limit of one wait at the persistent kernel's step barrier, in
- * microseconds (0 = default, 10 s).  When exceeded the kernel records a
+/* Wall-clock limit of one wait of the persistent kernel for the previous step,
+ * in microseconds (0 = default, 10 s).  When exceeded the kernel records a
  * timeout (see pat_check_device_status) and exits instead of waiting forever;
  * the operation's result is then undefined. */
 pat_status_t pat_set_barrier_timeout_us(uint32_t microseconds);

@@ -57,13 +57,18 @@ int order_now() {
 
 uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }
 
-// Persistent grid: at most this many workgroups per compute unit.  The
-// occupancy calculator's figure (7 per CU for these kernels on MI355X) was
-// not co-resident in practice -- the barrier timed out -- while up to 4 per
-// CU was; 2 leaves a wide margin.  0 means "the calculator's figure".
-int blocks_per_cu_cap() {
+// Persistent grid: at most this many workgroups per compute unit (0: as many
+// as the occupancy calculator allows).  The work-queue kernel needs no
+// co-residency, so this is a tuning knob, not a safety margin.  Each
+// workgroup pays a device-scope release and acquire per step, so small steps
+// run best on few workgroups and large ones on a full chip (measured on
+// MI355X: 2 per CU below 128 MiB per step, 4 below 2 GiB, then all).
+// PAT_PERSISTENT_BLOCKS_PER_CU overrides.
+int blocks_per_cu_cap(double bytes_per_step) {
   if (const char* e = std::getenv("PAT_PERSISTENT_BLOCKS_PER_CU")) return std::max(0, std::atoi(e));
-  return 2;
+  if (bytes_per_step < 128.0 * (1 << 20)) return 2;
+  if (bytes_per_step < 2048.0 * (1 << 20)) return 4;
+  return 0;
 }
 
 // Loads stream (nontemporal) when an operation moves at least this many bytes;
@@ -100,7 +105,8 @@ struct Plan {
   void** d_recv = nullptr;
   char* d_slots = nullptr;
   char* d_rootacc = nullptr;
-  unsigned* d_sync = nullptr;  // [0..1] barrier counters, [2] status
+  unsigned* d_sync = nullptr;  // persistent-kernel counters: [2] status, work queue from [4]
+  size_t sync_words = 0;
   int64_t slot_chunk_stride = 0, slot_rank_stride = 0, rootacc_stride = 0;
   std::vector<const void*> h_send;
   std::vector<void*> h_recv;
@@ -110,6 +116,7 @@ struct Plan {
   hipGraphExec_t graph[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};  // [vec][own_copy]
   int capacity[pat::kNumVariants][2] = {};
   bool nt_loads = true;
+  double alg_bytes = 0.0;  // algorithmic bytes of one operation
   int cus = 0;
   int64_t clock_khz = 0;
   size_t bytes = 0;          // device memory held (slots, accumulators, tables)
@@ -221,12 +228,14 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
   p->nt_loads = nt_loads_for(d.alg_bytes);
+  p->alg_bytes = d.alg_bytes;
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
   if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)round_up(size_t(d.piece_elems) * 4, 256);
   p->bytes = size_t(p->slot_rank_stride + p->rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
-             (p->steps[0].size() + p->steps[1].size()) * sizeof(pat::DevStep) + 2 * N * sizeof(void*) + 16;
+             (p->steps[0].size() + p->steps[1].size()) * sizeof(pat::DevStep) + 2 * N * sizeof(void*) +
+             pat::queue_words(std::max(p->steps[0].size(), p->steps[1].size())) * sizeof(unsigned);
   make_room(device, p->bytes);
 
   // On an allocation failure, release every other cached plan of this device
@@ -257,8 +266,9 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   if ((s = alloc((void**)&p->d_recv, N * sizeof(void*))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_slots, size_t(p->slot_rank_stride) * N)) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_rootacc, size_t(p->rootacc_stride) * N)) != PAT_OK) return s;
-  if ((s = alloc((void**)&p->d_sync, 4 * sizeof(unsigned))) != PAT_OK) return s;
-  HIP_TRY(hipMemset(p->d_sync, 0, 4 * sizeof(unsigned)));
+  p->sync_words = pat::queue_words(std::max(p->steps[0].size(), p->steps[1].size()));
+  if ((s = alloc((void**)&p->d_sync, p->sync_words * sizeof(unsigned))) != PAT_OK) return s;
+  HIP_TRY(hipMemset(p->d_sync, 0, p->sync_words * sizeof(unsigned)));
   if (const char* e = std::getenv("PAT_POISON_SLOTS")) {
     if (e[0] == '1') {
       if (p->d_slots) HIP_TRY(hipMemset(p->d_slots, 0xFF, size_t(p->slot_rank_stride) * N));
@@ -406,7 +416,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     plan->cus = cus;
   }
   cx.timeout_ticks = (int64_t)timeout_us_now() * plan->clock_khz / 1000;
-  cx.bar = plan->d_sync;
+  cx.queue = plan->d_sync;
   cx.status = plan->d_sync + 2;
 
   const pat::Variant var = variant_for(coll, dt, vec);
@@ -419,8 +429,9 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     int64_t most = 1;
     for (const auto& st : steps) most = std::max(most, st.items);
     int64_t cap = capacity;
-    if (const int per_cu = blocks_per_cu_cap()) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
-    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));
+    const double per_step = plan->alg_bytes / double(std::max<size_t>(1, steps.size()));
+    if (const int per_cu = blocks_per_cu_cap(per_step)) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));  // any size is safe
     if (const char* e = std::getenv("PAT_DEBUG"))
       if (e[0] == '1')
         std::fprintf(stderr, "[pat] persistent launch: capacity=%d cus=%d grid=%d steps=%d\n",
@@ -600,11 +611,11 @@ pat_status_t pat_check_device_status(hipStream_t stream) {
   for (auto& kv : g_plans) {
     Plan* p = kv.second.get();
     if (p->device != device) continue;
-    unsigned h[4] = {0, 0, 0, 0};
-    HIP_TRY(hipMemcpy(h, p->d_sync, sizeof(h), hipMemcpyDeviceToHost));
-    if (h[2]) {
+    unsigned st = 0;
+    HIP_TRY(hipMemcpy(&st, p->d_sync + 2, sizeof(st), hipMemcpyDeviceToHost));
+    if (st) {
       result = PAT_ERR_TIMEOUT;
-      HIP_TRY(hipMemset(p->d_sync, 0, sizeof(h)));
+      HIP_TRY(hipMemset(p->d_sync, 0, p->sync_words * sizeof(unsigned)));
     }
   }
   return result;

@@ -31,8 +31,9 @@
 //
 // Step order: steps depend on each other (a slot written at step s is read
 // at step s + 1).  Per-step launches get the ordering from the kernel
-// boundary; the persistent kernel uses a device-wide barrier whose fences
-// make every block's writes visible across the XCDs' separate L2 caches.
+// boundary; the persistent kernel orders its work queue by per-step
+// completion counters whose fences make every workgroup's writes visible
+// across the XCDs' separate L2 caches.
 
 #include <hip/hip_runtime.h>
 
@@ -396,62 +397,177 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
   for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
 }
 
-// Device-wide barrier for the persistent kernel.
-//  1. Every wave waits until its own stores are complete (acknowledged by this
-//     XCD's L2): a workgroup barrier alone does not wait for them.
-//  2. After the workgroup barrier, one thread counts in with an agent-scope
-//     release (one write-back of the XCD's L2, whose lines now include every
-//     wave's stores), then polls until all workgroups have arrived or the
-//     wall-clock limit passes, and takes an agent-scope acquire (invalidates
-//     this CU's L1 and the L2 lines other XCDs may have changed).
-//  3. A second workgroup barrier releases the other waves, whose loads come
-//     after the invalidation.
-// Returns false if the wait gave up (status bit set); the block then stops.
-__device__ bool grid_barrier(const KCtx& cx, unsigned target, int* s_ok) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+// Persistent execution: one launch per operation.  Step s has
+// G_s = min(grid, items_s) worker ids; a workgroup takes the next id of its
+// current step and processes items id, id + G_s, ...  Once every id of the
+// step has been taken it moves to the next step.  Before working on step s it
+// waits until all G_{s-1} ids of step s - 1 are done; step s - 1 done implies
+// every earlier step done, so each step sees exactly what a kernel boundary
+// would give it.
+//
+// No co-residency is needed: a workgroup enters step s only after every id of
+// step s - 1 was taken by a running workgroup, and those depend only on
+// earlier steps, so by induction over the steps all work completes whatever
+// the grid size.  The launch is a plain one, at full occupancy.
+//
+// Counters are spread over kShards cache lines per step: atomics on a single
+// address serialise (about 11 ns each on MI355X, 20 us for one round of 1792
+// workgroups), spread ones do not.  Id j*kShards + h lives in shard h; a
+// workgroup takes ids from shard blockIdx % kShards and, when that shard is
+// empty, looks at all shards before declaring the step fully taken.  An id
+// done counts in its shard's done counter; whoever completes a shard counts
+// it in the step's counter, so a step is done when that single word reaches
+// the number of non-empty shards, and waiters poll one word.
+//
+// Memory ordering across the XCDs' separate L2 caches:
+//  - finishing an id: every wave waits for its own stores (a workgroup
+//    barrier does not), then one thread counts the id done with an
+//    agent-scope release (one write-back of this XCD's L2); the shard's
+//    completer reads its counter with acquire, so its release on the step
+//    counter covers every id of the shard;
+//  - entering a step: one thread polls the previous step's counter, then
+//    takes an agent-scope acquire (invalidates this CU's L1 and stale L2
+//    lines) before a workgroup barrier lets the other waves load.
+// Every wait has a wall-clock limit; past it the status bit is set and the
+// workgroup stops (the operation's result is then undefined).  The last
+// workgroup out returns every counter to zero for the next launch.
+constexpr int kShards = 32;
+constexpr int kLineWords = 32;  // one 128-byte line per counter
+
+// Counter lines: [0, S*kShards) ids taken, [S*kShards, 2*S*kShards) ids done,
+// [2*S*kShards, 2*S*kShards + S) shards done per step, S = nsteps.
+__device__ __forceinline__ unsigned* queue_line(const KCtx& cx, int64_t line) {
+  return cx.queue + 4 + line * kLineWords;
+}
+__device__ __forceinline__ unsigned* taken_ctr(const KCtx& cx, int s, int h) {
+  return queue_line(cx, (int64_t)s * kShards + h);
+}
+__device__ __forceinline__ unsigned* done_ctr(const KCtx& cx, int s, int h) {
+  return queue_line(cx, ((int64_t)cx.nsteps + s) * kShards + h);
+}
+__device__ __forceinline__ unsigned* step_ctr(const KCtx& cx, int s) {
+  return queue_line(cx, 2 * (int64_t)cx.nsteps * kShards + s);
+}
+__device__ __forceinline__ int64_t shard_ids(int64_t G, int h) {
+  return G > h ? (G - h + kShards - 1) / kShards : 0;
+}
+__device__ __forceinline__ int64_t step_ids(const KCtx& cx, int s) {
+  const int64_t items = cx.steps[s].items;
+  return items < (int64_t)gridDim.x ? items : (int64_t)gridDim.x;
+}
+
+struct QueueShared {
+  int64_t id;
+  int flag;
+  unsigned vals[kShards];
+};
+
+// Next worker id of step s for this workgroup, or -1 once every id of the
+// step has been taken.  Called by all threads; the result is uniform.
+__device__ int64_t take_id(const KCtx& cx, int s, int64_t G, QueueShared* q) {
   if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(&cx.bar[0], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    const long long t0 = wall_clock64();
-    int ok = 1;
-    while ((int)(__hip_atomic_load(&cx.bar[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
-      __builtin_amdgcn_s_sleep(2);
-      if (wall_clock64() - t0 > cx.timeout_ticks) {
-        __hip_atomic_fetch_or(cx.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ok = 0;
-        break;
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    *s_ok = ok;
+    const int h = blockIdx.x % kShards;
+    const unsigned j = __hip_atomic_fetch_add(taken_ctr(cx, s, h), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    q->id = (int64_t)j < shard_ids(G, h) ? (int64_t)j * kShards + h : -1;
   }
   __syncthreads();
-  return *s_ok != 0;
+  int64_t id = q->id;
+  __syncthreads();
+  while (id == -1) {
+    if (threadIdx.x < kShards)
+      q->vals[threadIdx.x] = __hip_atomic_load(taken_ctr(cx, s, threadIdx.x), __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int64_t got = -2;  // every shard empty
+      for (int h = 0; h < kShards; ++h) {
+        if ((int64_t)q->vals[h] >= shard_ids(G, h)) continue;
+        const unsigned j = __hip_atomic_fetch_add(taken_ctr(cx, s, h), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((int64_t)j < shard_ids(G, h)) {
+          got = (int64_t)j * kShards + h;
+          break;
+        }
+        got = -1;  // lost a race for that shard: look again
+      }
+      q->id = got;
+    }
+    __syncthreads();
+    id = q->id;
+    __syncthreads();
+  }
+  return id < 0 ? -1 : id;
+}
+
+// Thread 0 counts worker id `id` of step s done.
+__device__ __forceinline__ void finish_id(const KCtx& cx, int s, int64_t G, int64_t id) {
+  const int h = (int)(id % kShards);
+  const unsigned before = __hip_atomic_fetch_add(done_ctr(cx, s, h), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  if ((int64_t)before + 1 == shard_ids(G, h))
+    __hip_atomic_fetch_add(step_ctr(cx, s), 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until every id of step s is done.  Returns false on timeout.
+__device__ bool wait_step(const KCtx& cx, int s, QueueShared* q) {
+  if (threadIdx.x == 0) {
+    const int64_t G = step_ids(cx, s);
+    const unsigned need = (unsigned)(G < kShards ? G : kShards);
+    const long long t0 = wall_clock64();
+    int f = 0;
+    for (;;) {
+      if (__hip_atomic_load(step_ctr(cx, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= need) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        f = 1;
+        break;
+      }
+      if (wall_clock64() - t0 > cx.timeout_ticks) {
+        __hip_atomic_fetch_or(cx.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        f = -1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    q->flag = f;
+  }
+  __syncthreads();
+  const int f = q->flag;
+  __syncthreads();
+  return f > 0;
 }
 
 template <class Op>
 __global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
-  __shared__ int s_ok;
-  unsigned target = 0;
-  bool ok = true;
-  for (int s = 0; s < cx.nsteps && ok; ++s) {
+  __shared__ QueueShared q;
+  int ready = 0;  // steps before `ready` are known done
+  for (int s = 0; s < cx.nsteps;) {
     const DevStep st = cx.steps[s];
-    for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
-    if (s + 1 < cx.nsteps) {
-      target += gridDim.x;
-      ok = grid_barrier(cx, target, &s_ok);
+    const int64_t G = step_ids(cx, s);
+    const int64_t w = take_id(cx, s, G, &q);
+    if (w < 0) {
+      ++s;  // every id of this step is taken
+      continue;
     }
+    if (s > ready) {
+      if (!wait_step(cx, s - 1, &q)) break;
+      ready = s;
+    }
+    for (int64_t item = w; item < st.items; item += G) Op::run(cx, st, item);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) finish_id(cx, s, G, w);
   }
-  // Leave the counters at zero for the next launch: the last block out
-  // (every block has passed every barrier by then) resets them.
+  // Leave the counters at zero: the last workgroup out (every other one has
+  // finished all of its work by then) resets them.
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned done =
-        __hip_atomic_fetch_add(&cx.bar[1], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u;
-    if (done == gridDim.x) {
-      __hip_atomic_store(&cx.bar[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&cx.bar[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+  if (threadIdx.x == 0)
+    q.flag = (__hip_atomic_fetch_add(&cx.queue[1], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u == gridDim.x);
+  __syncthreads();
+  if (q.flag) {
+    const int64_t n = (2 * (int64_t)kShards + 1) * cx.nsteps;
+    for (int64_t k = threadIdx.x; k < n; k += blockDim.x)
+      __hip_atomic_store(queue_line(cx, k), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_store(&cx.queue[1], 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -471,10 +587,8 @@ hipError_t launch_step_t(const KCtx& cx, const DevStep& st, hipStream_t stream) 
 
 template <class Op>
 hipError_t launch_persistent_t(const KCtx& cx, int grid, hipStream_t stream) {
-  KCtx local = cx;
-  void* args[] = {&local};
-  return hipLaunchCooperativeKernel((const void*)persistent_kernel<Op>, dim3(grid), dim3(kThreads), args, 0,
-                                    stream);
+  hipLaunchKernelGGL(persistent_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx);
+  return hipGetLastError();
 }
 
 template <class Op>

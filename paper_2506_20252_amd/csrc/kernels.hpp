@@ -31,10 +31,15 @@ struct KCtx {
   int32_t nsteps;             // launch-level steps (schedule steps x pieces)
   int32_t own_copy;           // all-gather: copy the own chunk (0 when in place)
   uint32_t pad0;
-  int64_t timeout_ticks;      // persistent barrier: wall-clock ticks to wait before giving up
-  unsigned* bar;              // [2] persistent barrier: arrivals, exits (zero between launches)
-  unsigned* status;           // [1] bit 0: a barrier timed out
+  int64_t timeout_ticks;      // persistent kernel: wall-clock ticks one wait may take before giving up
+  unsigned* queue;            // persistent kernel: [1] workgroups finished, then per step 32 sharded
+                              // "ids taken", 32 "ids done" and one "shards done" counter, 128 B apart
+                              // (zero between launches)
+  unsigned* status;           // bit 0: a persistent kernel's wait timed out
 };
+
+// Words of the persistent kernel's counter area for `nsteps` launch-level steps.
+inline size_t queue_words(size_t nsteps) { return 4 + (2 * 32 + 1) * nsteps * 32; }
 
 enum Variant : int {
   kAgVec = 0,   // all-gather, 16-byte units
@@ -56,6 +61,9 @@ int variant_tile(Variant v);
 // nt_loads: nontemporal (streaming) loads, for operations much larger than the
 // 256 MB Infinity Cache; plain loads let small operations hit in it.
 hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream);
+// Persistent execution: one launch of `grid` workgroups that take per-step
+// worker ids from device counters in step order.  Any grid size is safe (a
+// workgroup only waits on work that running workgroups already hold).
 hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream);
 // Workgroups of the persistent kernel that fit on the current device at once.
 hipError_t persistent_capacity(Variant v, bool nt_loads, int* blocks);
