@@ -37,12 +37,18 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 
 // Tuning knobs (compile time): vectors in flight per lane, nontemporal
 // (streaming) stores, and the XCD-aware work-item order.
 #ifndef PAT_UNROLL
 #define PAT_UNROLL 2
+#endif
+// bf16 reduce-scatter: 8-byte input vectors beside 16-byte float32 partials.
+#ifndef PAT_B16_UNROLL
+#define PAT_B16_UNROLL (2 * PAT_UNROLL)
 #endif
 // Stores always stream; the loads' hint is chosen per plan (launch argument).
 #ifndef PAT_NT_STORES
@@ -136,17 +142,24 @@ struct AgOp {
   };
 
   __device__ static Edge edge(const KCtx& cx, const DevStep& st, int r, int i) {
-    const DevEntry en = cx.entries[st.entry0 + i];
+    return edge_of(cx, st, r, cx.entries[st.entry0 + i]);
+  }
+
+  __device__ static Edge edge_of(const KCtx& cx, const DevStep& st, int r, const DevEntry& en) {
     const int c = wrap_sub(r, en.p, cx.N);
     const int peer = wrap_add(r, st.d, cx.N);
     const int64_t piece = st.e0 * cx.esize;
     const int64_t chunk = cx.count * cx.esize;
+    // Pointer-table reads happen whether or not the edge uses them, so that
+    // none of them sits in a branch of its own (and waits there).
+    const char* send_r = (const char*)cx.send[r];
+    char* recv_peer = (char*)cx.recv[peer];
+    char* recv_r = (char*)cx.recv[r];
     Edge e;
-    e.src = en.a == kUser ? (const char*)cx.send[r] + piece
-                          : cx.slots + r * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
-    e.dst = (char*)cx.recv[peer] + c * chunk + piece;
+    e.src = en.a == kUser ? send_r + piece : cx.slots + r * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.dst = recv_peer + c * chunk + piece;
     e.dst2 = en.b >= 0 ? cx.slots + peer * cx.slot_rank_stride + en.b * cx.slot_chunk_stride : nullptr;
-    e.dst3 = (st.first && en.p == 0 && cx.own_copy) ? (char*)cx.recv[r] + r * chunk + piece : nullptr;
+    e.dst3 = (st.first && en.p == 0 && cx.own_copy) ? recv_r + r * chunk + piece : nullptr;
     return e;
   }
 
@@ -178,19 +191,28 @@ struct AgOp {
     } else {
       const int64_t units = (int64_t)cx.N * st.k * st.V;
       const bool small = units < (int64_t(1) << 31);
+      // In phases (entries, then pointer tables, then data), so that each
+      // level of dependent loads is in flight for all U vectors at once.
       Edge e[U];
+      DevEntry en[U];
+      int rr[U];
       int64_t vv[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t g = item * kTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
         if (g < units) {
-          int r, i;
-          split_flat(g, st, &r, &i, &vv[j], small);
-          e[j] = edge(cx, st, r, i);
-          x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+          int i;
+          split_flat(g, st, &rr[j], &i, &vv[j], small);
+          en[j] = cx.entries[st.entry0 + i];
         }
       }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) e[j] = edge_of(cx, st, rr[j], en[j]);
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
 #pragma unroll
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) put(e[j], vv[j], x[j]);
@@ -239,7 +261,7 @@ struct TB16V {
   using acc_t = v4f;
   static constexpr int kInElem = 2;
   static constexpr bool kSeparateRoot = true;
-  static constexpr int kUnroll = 2 * PAT_UNROLL;  // 8-byte input vectors: same bytes in flight
+  static constexpr int kUnroll = PAT_B16_UNROLL;
   __device__ static acc_t widen(const in_t& x) {
     return v4f{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)};
   }
@@ -298,34 +320,43 @@ struct RsOp {
     bool dst_final;  // root's last receive (bf16): store rounded to the receive buffer
   };
 
-  __device__ static char* root(const KCtx& cx, const DevStep& st, int r) {
-    if (R::kSeparateRoot) return cx.rootacc + r * cx.rootacc_stride;
-    return (char*)cx.recv[r] + st.e0 * R::kInElem;
+  __device__ static Edge edge(const KCtx& cx, const DevStep& st, int r, int i) {
+    return edge_of(cx, st, r, cx.entries[st.entry0 + i]);
   }
 
-  __device__ static Edge edge(const KCtx& cx, const DevStep& st, int r, int i) {
-    const DevEntry en = cx.entries[st.entry0 + i];
+  __device__ static Edge edge_of(const KCtx& cx, const DevStep& st, int r, const DevEntry& en) {
     const int c = wrap_sub(r, en.p, cx.N);
     const int child = wrap_add(r, st.d, cx.N);
     const int64_t uoff = (c * cx.count + st.e0) * R::kInElem;
+    // Pointer-table reads happen whether or not the edge uses them, so that
+    // none of them sits in a branch of its own (and waits there).
+    const char* send_child = (const char*)cx.send[child];
+    const char* send_r = (const char*)cx.send[r];
+    char* const recv_r = (char*)cx.recv[r] + st.e0 * R::kInElem;
+    char* const root_acc = R::kSeparateRoot ? cx.rootacc + r * cx.rootacc_stride : recv_r;
+    char* const slots_r = cx.slots + r * cx.slot_rank_stride;
     Edge e;
     e.child_in = en.a == kUser;
-    e.child = e.child_in ? (const char*)cx.send[child] + uoff
-                         : cx.slots + child * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.child = e.child_in ? send_child + uoff : cx.slots + child * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
     e.own_in = en.b == kUser;
-    e.own = e.own_in ? (const char*)cx.send[r] + uoff
-            : en.b == kRoot ? root(cx, st, r)
-                            : cx.slots + r * cx.slot_rank_stride + en.b * cx.slot_chunk_stride;
+    e.own = e.own_in ? send_r + uoff : en.b == kRoot ? root_acc : slots_r + en.b * cx.slot_chunk_stride;
     e.dst_final = R::kSeparateRoot && en.c == kRootFinal;
-    e.dst = en.c >= 0 ? cx.slots + r * cx.slot_rank_stride + en.c * cx.slot_chunk_stride
-            : e.dst_final ? (char*)cx.recv[r] + st.e0 * R::kInElem
-                          : root(cx, st, r);
+    e.dst = en.c >= 0 ? slots_r + en.c * cx.slot_chunk_stride : e.dst_final ? recv_r : root_acc;
     return e;
   }
 
-  __device__ static acc_t load(const char* p, bool raw, int64_t v) {
-    if (raw) return R::widen(ldg<in_t, NTL>(p + v * (int64_t)sizeof(in_t)));
-    return ldg<acc_t, NTL>(p + v * (int64_t)sizeof(acc_t));
+  // int32 and float32: a raw input vector and an accumulator vector are alike.
+  static constexpr bool kSameVec = std::is_same<in_t, acc_t>::value;
+
+  template <bool RAW>
+  using vec_t = typename std::conditional<RAW, in_t, acc_t>::type;
+
+  template <bool RAW>
+  __device__ static acc_t to_acc(const vec_t<RAW>& x) {
+    if constexpr (RAW)
+      return R::widen(x);
+    else
+      return x;
   }
 
   __device__ static void store(const Edge& e, int64_t v, const acc_t& x) {
@@ -335,47 +366,116 @@ struct RsOp {
       stg(e.dst + v * (int64_t)sizeof(acc_t), x);
   }
 
+  // One tile of one edge whose operand kinds are known: every load is issued
+  // before any value is used, so a lane keeps 2U loads in flight (a raw bf16
+  // input widened right after its load would wait for each load in turn).
+  template <bool OWN_RAW, bool CHILD_RAW>
+  __device__ static void tile(const Edge& e, int64_t tile_idx, int64_t V) {
+    vec_t<OWN_RAW> a[U];
+    vec_t<CHILD_RAW> b[U];
+    const int64_t v0 = tile_idx * kTile + threadIdx.x;
+    if ((tile_idx + 1) * kTile <= V) {
+      // Full tile (uniform): straight-line code, no per-lane guards.
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t v = v0 + j * kThreads;
+        a[j] = ldg<vec_t<OWN_RAW>, NTL>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
+        b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        store(e, v0 + j * kThreads, R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j])));
+      return;
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int64_t v = v0 + j * kThreads;
+      if (v < V) {
+        a[j] = ldg<vec_t<OWN_RAW>, NTL>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
+        b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int64_t v = v0 + j * kThreads;
+      if (v < V) store(e, v, R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j])));
+    }
+  }
+
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
-    acc_t a[U], b[U];
     if (st.tiles_per_edge > 0) {
       int r, i;
-      int64_t tile;
-      split_tile(item, st, &r, &i, &tile);
+      int64_t tile_idx;
+      split_tile(item, st, &r, &i, &tile_idx);
       const Edge e = edge(cx, st, r, i);
-      const int64_t v0 = tile * kTile + threadIdx.x;
-#pragma unroll
-      for (int j = 0; j < U; ++j) {
-        const int64_t v = v0 + j * kThreads;
-        if (v < st.V) {
-          a[j] = load(e.own, e.own_in, v);
-          b[j] = load(e.child, e.child_in, v);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < U; ++j) {
-        const int64_t v = v0 + j * kThreads;
-        if (v < st.V) store(e, v, R::add(a[j], b[j]));
+      if constexpr (kSameVec) {
+        tile<false, false>(e, tile_idx, st.V);
+      } else if (e.own_in) {
+        if (e.child_in)
+          tile<true, true>(e, tile_idx, st.V);
+        else
+          tile<true, false>(e, tile_idx, st.V);
+      } else {
+        if (e.child_in)
+          tile<false, true>(e, tile_idx, st.V);
+        else
+          tile<false, false>(e, tile_idx, st.V);
       }
     } else {
+      // Packed: each lane's vectors may belong to different edges, so both
+      // kinds of load are predicated per lane; conversions again come after
+      // every load has been issued.
       const int64_t units = (int64_t)cx.N * st.k * st.V;
       const bool small = units < (int64_t(1) << 31);
+      // In phases (entries, then pointer tables, then data), so that each
+      // level of dependent loads is in flight for all U vectors at once.
       Edge e[U];
+      DevEntry en[U];
+      int rr[U];
       int64_t vv[U];
+      in_t ra[U], rb[U];
+      acc_t xa[U], xb[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t g = item * kTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
         if (g < units) {
-          int r, i;
-          split_flat(g, st, &r, &i, &vv[j], small);
-          e[j] = edge(cx, st, r, i);
-          a[j] = load(e[j].own, e[j].own_in, vv[j]);
-          b[j] = load(e[j].child, e[j].child_in, vv[j]);
+          int i;
+          split_flat(g, st, &rr[j], &i, &vv[j], small);
+          en[j] = cx.entries[st.entry0 + i];
         }
       }
 #pragma unroll
       for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) store(e[j], vv[j], R::add(a[j], b[j]));
+        if (vv[j] >= 0) e[j] = edge_of(cx, st, rr[j], en[j]);
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        if (vv[j] >= 0) {
+          if constexpr (kSameVec) {
+            xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+            xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+          } else {
+            if (e[j].own_in)
+              ra[j] = ldg<in_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
+            else
+              xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+            if (e[j].child_in)
+              rb[j] = ldg<in_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
+            else
+              xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) {
+          acc_t a = xa[j], b = xb[j];
+          if constexpr (!kSameVec) {
+            if (e[j].own_in) a = R::widen(ra[j]);
+            if (e[j].child_in) b = R::widen(rb[j]);
+          }
+          store(e[j], vv[j], R::add(a, b));
+        }
     }
   }
 };
