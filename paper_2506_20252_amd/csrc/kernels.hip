@@ -118,6 +118,12 @@ __device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r,
   }
 }
 
+// Waits for every outstanding memory access of this lane.  Used between a
+// load phase and stores that sit in per-lane branches: there the compiler
+// cannot count which loads a store still needs and waits before each store
+// for all earlier ones, stores included; one wait up front avoids that.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Split a tiled work item into (rank, entry, tile).
 __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int* r, int* i, int64_t* tile) {
   const int64_t e = item / st.tiles_per_edge;
@@ -178,11 +184,29 @@ struct AgOp {
       split_tile(item, st, &r, &i, &tile);
       const Edge e = edge(cx, st, r, i);
       const int64_t v0 = tile * kTile + threadIdx.x;
+      if ((tile + 1) * kTile <= st.V) {
+        // Full tile (uniform): straight-line loads, then one store loop per
+        // destination, so no store waits for another store.
+#pragma unroll
+        for (int j = 0; j < U; ++j) x[j] = ldg<Unit, NTL>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
+#pragma unroll
+        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        if (e.dst2) {
+#pragma unroll
+          for (int j = 0; j < U; ++j) stg(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        }
+        if (e.dst3) {
+#pragma unroll
+          for (int j = 0; j < U; ++j) stg(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        }
+        return;
+      }
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t v = v0 + j * kThreads;
         if (v < st.V) x[j] = ldg<Unit, NTL>(e.src + v * (int64_t)sizeof(Unit));
       }
+      wait_loads();
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t v = v0 + j * kThreads;
@@ -213,6 +237,7 @@ struct AgOp {
 #pragma unroll
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+      wait_loads();
 #pragma unroll
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) put(e[j], vv[j], x[j]);
@@ -382,9 +407,16 @@ struct RsOp {
         a[j] = ldg<vec_t<OWN_RAW>, NTL>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
         b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
+      acc_t sum[U];
 #pragma unroll
-      for (int j = 0; j < U; ++j)
-        store(e, v0 + j * kThreads, R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j])));
+      for (int j = 0; j < U; ++j) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
+      if (R::kSeparateRoot && e.dst_final) {
+#pragma unroll
+        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
+      } else {
+#pragma unroll
+        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
+      }
       return;
     }
 #pragma unroll
@@ -395,10 +427,14 @@ struct RsOp {
         b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
     }
+    acc_t sum[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (v0 + j * kThreads < V) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       const int64_t v = v0 + j * kThreads;
-      if (v < V) store(e, v, R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j])));
+      if (v < V) store(e, v, sum[j]);
     }
   }
 
@@ -466,6 +502,7 @@ struct RsOp {
           }
         }
       }
+      acc_t sum[U];
 #pragma unroll
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) {
@@ -474,8 +511,12 @@ struct RsOp {
             if (e[j].own_in) a = R::widen(ra[j]);
             if (e[j].child_in) b = R::widen(rb[j]);
           }
-          store(e[j], vv[j], R::add(a, b));
+          sum[j] = R::add(a, b);
         }
+      wait_loads();
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) store(e[j], vv[j], sum[j]);
     }
   }
 };
