@@ -147,6 +147,24 @@ int pat_get_linear_order(void);
 pat_status_t pat_set_exec_mode(int mode);
 int pat_get_exec_mode(void);
 
+/*
+ * Fusion of the schedule's top part (stream and graph modes).  In the top t
+ * steps (the fully aggregated distances, section "The PAT algorithm") every
+ * intermediate-buffer entry serves a single tree, so one workgroup per (tree,
+ * tile of its chunk) can run all of them with workgroup barriers instead of
+ * one kernel per step.  The edges, bytes and summation order are unchanged.
+ * A workgroup runs its tree's steps one after another, so wide steps (many
+ * chunks per rank) are better left to one kernel each.  AUTO (the default, or
+ * the PAT_TOP_FUSION environment variable: auto | on | off) fuses the far end
+ * of the top part, the steps in which one tree's edges over one tile of its
+ * chunk amount to at most 1024 vectors, when there are two or more such steps;
+ * ON fuses the whole top part whenever it has two or more steps.  Neither
+ * fuses a chunk that is split into pieces.
+ */
+typedef enum { PAT_FUSION_AUTO = 0, PAT_FUSION_OFF = 1, PAT_FUSION_ON = 2 } pat_fusion_t;
+pat_status_t pat_set_top_fusion(int mode);
+int pat_get_top_fusion(void);
+
 /* Wall-clock limit of one wait of the persistent kernel for the previous step,
  * in microseconds (0 = default, 10 s).  When exceeded the kernel records a
  * timeout (see pat_check_device_status) and exits instead of waiting forever;

@@ -28,6 +28,7 @@ size_t g_budget = 0;     // 0: default
 int g_mode = -1;         // -1: environment / default
 uint32_t g_timeout_us = 0;  // 0: default
 int g_order = -1;           // -1: environment / default (far-first)
+int g_fusion = -1;          // -1: environment / default (auto)
 std::atomic<int> g_last_hip{0};
 
 size_t budget_now() {
@@ -53,6 +54,37 @@ int order_now() {
   if (const char* e = std::getenv("PAT_LINEAR_ORDER"))
     if (!std::strcmp(e, "close")) return pat::kCloseFirst;
   return pat::kFarFirst;
+}
+
+int fusion_now() {
+  if (g_fusion >= 0) return g_fusion;
+  if (const char* e = std::getenv("PAT_TOP_FUSION")) {
+    if (!std::strcmp(e, "on")) return PAT_FUSION_ON;
+    if (!std::strcmp(e, "off")) return PAT_FUSION_OFF;
+  }
+  return PAT_FUSION_AUTO;
+}
+
+// PAT_FUSION_AUTO fuses the far end of the top part: the steps whose edges
+// of one tree, times the vectors of one tile, fit this many vectors (about
+// one load round per lane).  Wider steps keep a kernel each, which spreads
+// their edges over the whole chip.  PAT_TREE_FUSE_VECS overrides.
+int64_t tree_fuse_vecs() {
+  if (const char* e = std::getenv("PAT_TREE_FUSE_VECS")) {
+    const long long v = std::atoll(e);
+    if (v > 0) return v;
+  }
+  return 1024;
+}
+
+// Vectors of a chunk per workgroup of the fused top part (PAT_TREE_TILE
+// overrides, for tuning).
+int64_t tree_tile_vecs() {
+  if (const char* e = std::getenv("PAT_TREE_TILE")) {
+    const long long v = std::atoll(e);
+    if (v > 0) return v;
+  }
+  return 2048;
 }
 
 uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }
@@ -113,7 +145,8 @@ struct Plan {
   void** pinned = nullptr;  // 2N pointers staged for upload
   hipEvent_t upload_done = nullptr;
   bool upload_pending = false;
-  hipGraphExec_t graph[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};  // [vec][own_copy]
+  hipGraphExec_t graph[2][2][2] = {};  // [vec][own_copy][top part fused]
+  int top_s0 = 0, top_s1 = 0;          // launch-level steps of the top part (empty: not fusable)
   int capacity[pat::kNumVariants][2] = {};
   bool nt_loads = true;
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
@@ -125,9 +158,10 @@ struct Plan {
   uint64_t last_use = 0;     // LRU stamp
 
   ~Plan() {
-    for (auto& row : graph)
-      for (auto& g : row)
-        if (g) (void)hipGraphExecDestroy(g);
+    for (auto& plane : graph)
+      for (auto& row : plane)
+        for (auto& g : row)
+          if (g) (void)hipGraphExecDestroy(g);
     if (done) (void)hipEventDestroy(done);
     if (upload_done) (void)hipEventDestroy(upload_done);
     if (pinned) (void)hipHostFree(pinned);
@@ -229,6 +263,13 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
   p->nt_loads = nt_loads_for(d.alg_bytes);
   p->alg_bytes = d.alg_bytes;
+  // The top part: the first t steps of the all-gather order, the last t of
+  // the reduce-scatter's (one piece only).
+  if (d.pieces == 1 && d.sched.t >= 2) {
+    const int ns = (int)d.exec.size(), t = d.sched.t;
+    p->top_s0 = coll == 0 ? 0 : ns - t;
+    p->top_s1 = coll == 0 ? t : ns;
+  }
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
@@ -437,29 +478,64 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
         std::fprintf(stderr, "[pat] persistent launch: capacity=%d cus=%d grid=%d steps=%d\n",
                      capacity, plan->cus, grid, cx.nsteps);
     HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
-  } else if (mode == PAT_EXEC_STREAM) {
-    for (size_t s = 0; s < steps.size(); ++s) HIP_TRY(pat::launch_step(var, plan->nt_loads, cx, steps[s], stream));
   } else {
-    hipGraphExec_t& exec = plan->graph[vi][cx.own_copy];
-    if (!exec) {
-      hipStream_t cs = nullptr;
-      HIP_TRY(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
-      hipGraph_t g = nullptr;
-      hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
-      for (size_t s = 0; e == hipSuccess && s < steps.size(); ++s)
-        e = pat::launch_step(var, plan->nt_loads, cx, steps[s], cs);
-      const hipError_t e2 = hipStreamEndCapture(cs, &g);
-      if (e == hipSuccess) e = e2;
-      if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);
-      if (g) (void)hipGraphDestroy(g);
-      (void)hipStreamDestroy(cs);
-      if (e != hipSuccess) {
-        exec = nullptr;
-        g_last_hip.store((int)e);
-        return PAT_ERR_HIP;
+    // Stream and graph modes: one kernel per step, except that the top part
+    // may run as one fused launch.
+    const int fusion = fusion_now();
+    pat::TreeRange tr{};
+    if (plan->top_s1 > plan->top_s0 && fusion != PAT_FUSION_OFF) {
+      const int64_t V = steps[plan->top_s0].V;
+      tr.s0 = plan->top_s0;
+      tr.s1 = plan->top_s1;
+      tr.tile_vecs = std::min<int64_t>(V, tree_tile_vecs());
+      tr.tiles = (V + tr.tile_vecs - 1) / tr.tile_vecs;
+      if (fusion == PAT_FUSION_AUTO) {
+        // Keep only the narrow far end: the reduce-scatter's last steps, the
+        // all-gather's first (their chunks per rank grow toward the middle).
+        const int64_t cap = tree_fuse_vecs();
+        if (coll == 1)
+          while (tr.s0 < tr.s1 && int64_t(steps[tr.s0].k) * tr.tile_vecs > cap) ++tr.s0;
+        else
+          while (tr.s1 > tr.s0 && int64_t(steps[tr.s1 - 1].k) * tr.tile_vecs > cap) --tr.s1;
       }
     }
-    HIP_TRY(hipGraphLaunch(exec, stream));
+    const bool fuse = tr.s1 - tr.s0 >= 2;
+    auto enqueue = [&](hipStream_t q) -> hipError_t {
+      for (int s = 0; s < (int)steps.size(); ++s) {
+        if (fuse && s == tr.s0) {
+          const hipError_t e = pat::launch_tree(var, plan->nt_loads, cx, tr, q);
+          if (e != hipSuccess) return e;
+          s = tr.s1 - 1;
+          continue;
+        }
+        const hipError_t e = pat::launch_step(var, plan->nt_loads, cx, steps[s], q);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
+    };
+    if (mode == PAT_EXEC_STREAM) {
+      HIP_TRY(enqueue(stream));
+    } else {
+      hipGraphExec_t& exec = plan->graph[vi][cx.own_copy][fuse ? 1 : 0];
+      if (!exec) {
+        hipStream_t cs = nullptr;
+        HIP_TRY(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+        hipGraph_t g = nullptr;
+        hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+        if (e == hipSuccess) e = enqueue(cs);
+        const hipError_t e2 = hipStreamEndCapture(cs, &g);
+        if (e == hipSuccess) e = e2;
+        if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);
+        if (g) (void)hipGraphDestroy(g);
+        (void)hipStreamDestroy(cs);
+        if (e != hipSuccess) {
+          exec = nullptr;
+          g_last_hip.store((int)e);
+          return PAT_ERR_HIP;
+        }
+      }
+      HIP_TRY(hipGraphLaunch(exec, stream));
+    }
   }
   HIP_TRY(hipEventRecord(plan->done, stream));
   plan->used = true;
@@ -519,6 +595,18 @@ pat_status_t pat_set_exec_mode(int mode) {
 int pat_get_exec_mode(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   return mode_now();
+}
+
+pat_status_t pat_set_top_fusion(int mode) {
+  if (mode < PAT_FUSION_AUTO || mode > PAT_FUSION_ON) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_fusion = mode;
+  return PAT_OK;
+}
+
+int pat_get_top_fusion(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  return fusion_now();
 }
 
 pat_status_t pat_set_linear_order(int order) {

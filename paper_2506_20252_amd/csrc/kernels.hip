@@ -132,12 +132,39 @@ __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int*
   *i = (int)(e - (int64_t)(*r) * st.k);
 }
 
+// One step of one tree in a fused top part: the pairs (entry i, vector v)
+// with i < k and v in [t0, t0 + TV), flattened vector-fastest so that lanes
+// sweep each edge's tile contiguously, U pairs per lane at a time.
+template <class Op>
+__device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+  constexpr int U = Op::U;
+  const int64_t n = (int64_t)st.k * TV;
+  for (int64_t base = 0; base < n; base += (int64_t)kThreads * U) {
+    int rr[U], ii[U];
+    int64_t vv[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int64_t f = base + j * kThreads + threadIdx.x;
+      vv[j] = -1;
+      rr[j] = c;
+      ii[j] = 0;
+      if (f < n) {
+        const int64_t i = f / TV;
+        ii[j] = (int)i;
+        vv[j] = t0 + (f - i * TV);
+      }
+    }
+    Op::template batch<true>(cx, st, rr, ii, vv);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // All-gather
 // ---------------------------------------------------------------------------
 
-template <typename Unit, int U, bool NTL>
+template <typename Unit, int kU, bool NTL>
 struct AgOp {
+  static constexpr int U = kU;
   static constexpr int kTile = kThreads * U;
 
   struct Edge {
@@ -215,33 +242,47 @@ struct AgOp {
     } else {
       const int64_t units = (int64_t)cx.N * st.k * st.V;
       const bool small = units < (int64_t(1) << 31);
-      // In phases (entries, then pointer tables, then data), so that each
-      // level of dependent loads is in flight for all U vectors at once.
-      Edge e[U];
-      DevEntry en[U];
-      int rr[U];
+      int rr[U], ii[U];
       int64_t vv[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t g = item * kTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
-        if (g < units) {
-          int i;
-          split_flat(g, st, &rr[j], &i, &vv[j], small);
-          en[j] = cx.entries[st.entry0 + i];
-        }
+        if (g < units) split_flat(g, st, &rr[j], &ii[j], &vv[j], small);
       }
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) e[j] = edge_of(cx, st, rr[j], en[j]);
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
-      wait_loads();
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) put(e[j], vv[j], x[j]);
+      batch<false>(cx, st, rr, ii, vv);
     }
+  }
+
+  // U vectors per lane, each given as (rank, entry, vector), or (tree, entry,
+  // vector) when TREE (the acting rank is then tree + the entry's position);
+  // vv[j] < 0 marks an unused slot.  In phases (entries, then pointer tables,
+  // then data), so that each level of dependent loads is in flight for all U
+  // vectors at once.
+  template <bool TREE>
+  __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
+                               const int64_t (&vv)[U]) {
+    Unit x[U];
+    Edge e[U];
+    DevEntry en[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+    wait_loads();
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) put(e[j], vv[j], x[j]);
+  }
+
+  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+    tree_step_impl<AgOp>(cx, st, c, t0, TV);
   }
 };
 
@@ -458,66 +499,78 @@ struct RsOp {
           tile<false, false>(e, tile_idx, st.V);
       }
     } else {
-      // Packed: each lane's vectors may belong to different edges, so both
-      // kinds of load are predicated per lane; conversions again come after
-      // every load has been issued.
       const int64_t units = (int64_t)cx.N * st.k * st.V;
       const bool small = units < (int64_t(1) << 31);
-      // In phases (entries, then pointer tables, then data), so that each
-      // level of dependent loads is in flight for all U vectors at once.
-      Edge e[U];
-      DevEntry en[U];
-      int rr[U];
+      int rr[U], ii[U];
       int64_t vv[U];
-      in_t ra[U], rb[U];
-      acc_t xa[U], xb[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t g = item * kTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
-        if (g < units) {
-          int i;
-          split_flat(g, st, &rr[j], &i, &vv[j], small);
-          en[j] = cx.entries[st.entry0 + i];
-        }
+        if (g < units) split_flat(g, st, &rr[j], &ii[j], &vv[j], small);
       }
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) e[j] = edge_of(cx, st, rr[j], en[j]);
-#pragma unroll
-      for (int j = 0; j < U; ++j) {
-        if (vv[j] >= 0) {
-          if constexpr (kSameVec) {
-            xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
-            xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
-          } else {
-            if (e[j].own_in)
-              ra[j] = ldg<in_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
-            else
-              xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
-            if (e[j].child_in)
-              rb[j] = ldg<in_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
-            else
-              xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
-          }
-        }
-      }
-      acc_t sum[U];
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) {
-          acc_t a = xa[j], b = xb[j];
-          if constexpr (!kSameVec) {
-            if (e[j].own_in) a = R::widen(ra[j]);
-            if (e[j].child_in) b = R::widen(rb[j]);
-          }
-          sum[j] = R::add(a, b);
-        }
-      wait_loads();
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (vv[j] >= 0) store(e[j], vv[j], sum[j]);
+      batch<false>(cx, st, rr, ii, vv);
     }
+  }
+
+  // U vectors per lane, each given as (rank, entry, vector), or (tree, entry,
+  // vector) when TREE (the acting rank is then tree + the entry's position);
+  // vv[j] < 0 marks an unused slot.  Each lane's vectors may belong to
+  // different edges, so both kinds of load are predicated per lane.  In phases
+  // (entries, then pointer tables, then data), so that each level of
+  // dependent loads is in flight for all U vectors at once; conversions come
+  // after every load has been issued.
+  template <bool TREE>
+  __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
+                               const int64_t (&vv)[U]) {
+    Edge e[U];
+    DevEntry en[U];
+    in_t ra[U], rb[U];
+    acc_t xa[U], xb[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      if (vv[j] >= 0) {
+        if constexpr (kSameVec) {
+          xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+          xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+        } else {
+          if (e[j].own_in)
+            ra[j] = ldg<in_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
+          else
+            xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+          if (e[j].child_in)
+            rb[j] = ldg<in_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
+          else
+            xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+        }
+      }
+    }
+    acc_t sum[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) {
+        acc_t a = xa[j], b = xb[j];
+        if constexpr (!kSameVec) {
+          if (e[j].own_in) a = R::widen(ra[j]);
+          if (e[j].child_in) b = R::widen(rb[j]);
+        }
+        sum[j] = R::add(a, b);
+      }
+    wait_loads();
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      if (vv[j] >= 0) store(e[j], vv[j], sum[j]);
+  }
+
+  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+    tree_step_impl<RsOp>(cx, st, c, t0, TV);
   }
 };
 
@@ -536,6 +589,28 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
     return;
   }
   for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
+}
+
+// Fused top part of the schedule: one workgroup per (tree, tile of its
+// chunk) runs the launch-level steps s0 .. s1 - 1 in order.  In the top part
+// every slot entry is used once and by one tree only, so the data a step of
+// tree c reads was written by an earlier step of tree c: by this workgroup.
+// A workgroup barrier between steps then replaces the kernel boundary; each
+// wave first waits for its own stores.
+template <class Op>
+__global__ __launch_bounds__(kThreads) void tree_kernel(KCtx cx, TreeRange tr) {
+  const int c = (int)(blockIdx.x / tr.tiles);
+  const int64_t tile = (int64_t)blockIdx.x - (int64_t)c * tr.tiles;
+  const int64_t t0 = tile * tr.tile_vecs;
+  for (int s = tr.s0; s < tr.s1; ++s) {
+    const DevStep st = cx.steps[s];
+    const int64_t left = st.V - t0;
+    Op::tree_step(cx, st, c, t0, left < tr.tile_vecs ? left : tr.tile_vecs);
+    if (s + 1 < tr.s1) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+  }
 }
 
 // Persistent execution: one launch per operation.  Step s has
@@ -797,6 +872,21 @@ hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& 
 #define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, stream)
   PAT_DISPATCH(v, nt_loads, PAT_STEP)
 #undef PAT_STEP
+}
+
+template <class Op>
+hipError_t launch_tree_t(const KCtx& cx, const TreeRange& tr, hipStream_t stream) {
+  const int64_t grid = (int64_t)cx.N * tr.tiles;
+  if (tr.s1 <= tr.s0 || grid <= 0) return hipSuccess;
+  if (grid >= (int64_t(1) << 31) || tr.tile_vecs <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(tree_kernel<Op>, dim3((unsigned)grid), dim3(kThreads), 0, stream, cx, tr);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree(Variant v, bool nt_loads, const KCtx& cx, const TreeRange& tr, hipStream_t stream) {
+#define PAT_TREE(OP) launch_tree_t<PAT_UNPAREN OP>(cx, tr, stream)
+  PAT_DISPATCH(v, nt_loads, PAT_TREE)
+#undef PAT_TREE
 }
 
 hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream) {

@@ -61,6 +61,14 @@ int variant_tile(Variant v);
 // nt_loads: nontemporal (streaming) loads, for operations much larger than the
 // 256 MB Infinity Cache; plain loads let small operations hit in it.
 hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream);
+// Fused top part: launch-level steps [s0, s1) of one piece, run by one
+// workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
+struct TreeRange {
+  int32_t s0, s1;
+  int64_t tile_vecs;
+  int64_t tiles;
+};
+hipError_t launch_tree(Variant v, bool nt_loads, const KCtx& cx, const TreeRange& tr, hipStream_t stream);
 // Persistent execution: one launch of `grid` workgroups that take per-step
 // worker ids from device counters in step order.  Any grid size is safe (a
 // workgroup only waits on work that running workgroups already hold).

@@ -44,10 +44,16 @@ PAT_LINEAR_FAR_FIRST = 0
 PAT_LINEAR_CLOSE_FIRST = 1
 ORDERS = {"far": PAT_LINEAR_FAR_FIRST, "close": PAT_LINEAR_CLOSE_FIRST}
 
+PAT_FUSION_AUTO = 0
+PAT_FUSION_OFF = 1
+PAT_FUSION_ON = 2
+FUSIONS = {"auto": PAT_FUSION_AUTO, "off": PAT_FUSION_OFF, "on": PAT_FUSION_ON}
+
 # Every function include/pat.h declares.
 EXPORTS = (
     "pat_allgather", "pat_reducescatter", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
+    "pat_set_top_fusion", "pat_get_top_fusion",
     "pat_set_barrier_timeout_us", "pat_plan_info",
     "pat_plan_steps", "pat_cache_stats", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
     "pat_finalize",
@@ -97,6 +103,8 @@ def lib():
             "pat_get_exec_mode": ([], ctypes.c_int),
             "pat_set_linear_order": ([ctypes.c_int], ctypes.c_int),
             "pat_get_linear_order": ([], ctypes.c_int),
+            "pat_set_top_fusion": ([ctypes.c_int], ctypes.c_int),
+            "pat_get_top_fusion": ([], ctypes.c_int),
             "pat_set_barrier_timeout_us": ([ctypes.c_uint32], ctypes.c_int),
             "pat_plan_info": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                                ctypes.POINTER(pat_plan_info_t)], ctypes.c_int),
@@ -175,6 +183,14 @@ def pat_set_exec_mode(mode):
 
 def pat_get_exec_mode():
     return int(lib().pat_get_exec_mode())
+
+
+def pat_set_top_fusion(mode):
+    return lib().pat_set_top_fusion(FUSIONS[mode] if isinstance(mode, str) else int(mode))
+
+
+def pat_get_top_fusion():
+    return int(lib().pat_get_top_fusion())
 
 
 def pat_set_linear_order(order):

@@ -184,3 +184,66 @@ def test_symbolic_execution_of_library_tables(n, order):
     finally:
         pat.pat_set_buffer_bytes(0)
         pat.pat_set_linear_order("far")
+
+
+def _slot_trees(coll, n, steps, entries, lo, hi):
+    """(rank, slot entry) -> set of trees that launch-level steps [lo, hi) touch there."""
+    use = {}
+    j = 0
+    for s, (d, k) in enumerate(steps):
+        if lo <= s < hi:
+            for (p, a, b, c) in entries[j:j + k]:
+                for r in range(n):
+                    tree = (r - p) % n
+                    if coll == pat.PAT_REDUCESCATTER:
+                        touched = [((r + d) % n, a), (r, b), (r, c)]
+                    else:
+                        touched = [(r, a), ((r + d) % n, b)]
+                    for rank, slot in touched:
+                        if slot >= 0:
+                            use.setdefault((rank, slot), set()).add(tree)
+        j += k
+    return use
+
+
+@pytest.mark.parametrize("order", ["far", "close"])
+@pytest.mark.parametrize("n", [3, 4, 5, 7, 8, 9, 16, 24, 33, 64, 100, 129])
+def test_top_part_slots_serve_one_tree(n, order):
+    """What fusing the top part relies on: in the top t steps (the first t of
+    the all-gather, the last t of the reduce-scatter) every intermediate-buffer
+    entry of every rank holds chunks of one tree only, so a workgroup that owns
+    a tree may run those steps without waiting for other trees.  The linear
+    part, by contrast, reuses entries across trees once T < 2^(L-1)."""
+    count = 64
+    pat.check(pat.pat_set_linear_order(order))
+    try:
+        saw_linear_reuse = False
+        L = opat.ceil_log2(n)
+        for t in range(1, max(L, 1)):
+            pat.pat_set_buffer_bytes(budget_for(n, t, count * 4))
+            for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+                st, info = pat.pat_plan_info(coll, n, count, "float32")
+                assert st == pat.PAT_OK and info["pieces"] == 1
+                _, steps, entries = library_steps(coll, n, count, "float32")
+                ns, tt = len(steps), info["t"]
+                lo, hi = (0, tt) if coll == pat.PAT_ALLGATHER else (ns - tt, ns)
+                assert all(d >= 1 << (L - tt) for d, _ in steps[lo:hi])  # the fully aggregated distances
+                top = _slot_trees(coll, n, steps, entries, lo, hi)
+                assert all(len(trees) == 1 for trees in top.values()), (coll, t)
+                rest = (hi, ns) if coll == pat.PAT_ALLGATHER else (0, lo)
+                lin = _slot_trees(coll, n, steps, entries, *rest)
+                saw_linear_reuse |= any(len(trees) > 1 for trees in lin.values())
+        if L >= 4:  # t = 1 leaves sub-trees of span >= 8, whose distance-2 entries serve two trees
+            assert saw_linear_reuse
+    finally:
+        pat.pat_set_buffer_bytes(0)
+        pat.pat_set_linear_order("far")
+
+
+def test_top_fusion_setting_roundtrip():
+    assert pat.pat_get_top_fusion() == pat.PAT_FUSION_AUTO
+    for m in ("on", "off", "auto"):
+        assert pat.pat_set_top_fusion(m) == pat.PAT_OK
+        assert pat.pat_get_top_fusion() == pat.FUSIONS[m]
+    assert pat.pat_set_top_fusion(7) == pat.PAT_ERR_INVALID_ARGUMENT
+    assert pat.pat_get_top_fusion() == pat.PAT_FUSION_AUTO
