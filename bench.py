@@ -161,6 +161,7 @@ def small_size_latency(reps=200):
         st, info = pat.pat_plan_info(code, n, count, "float32")
         out[f"{coll}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
         out["steps"] = info["steps"]
+        out[f"{coll}_launches"] = info["launches_per_op"]  # the top part's far steps run as one launch
         del send, recv, S, R
     torch.cuda.empty_cache()
     return out
@@ -211,6 +212,7 @@ def other_workloads(reps=50):
         sec = e0.elapsed_time(e1) / 1e3 / reps
         st, info = pat.pat_plan_info(code, n, count, dtype)
         rows.append({"workload": desc, "us": round(sec * 1e6, 2), "steps": info["steps"],
+                     "launches": info["launches_per_op"],
                      "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
                      "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
         del send, recv, S, R
@@ -270,6 +272,7 @@ def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
         pat.check(pat.pat_check_device_status(stream))
         sec = e0.elapsed_time(e1) / 1e3 / reps
         rows.append({"budget_bytes": budget, "T": info["T"], "steps": info["steps"],
+                     "launches": info["launches_per_op"],
                      "slot_bytes_per_rank": info["slot_bytes_per_rank"], "us": round(sec * 1e6, 2),
                      "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
                      "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
@@ -383,7 +386,7 @@ def main():
     sec = ms / 1e3
 
     bus_per_rank = info["bus_bytes_per_rank"]
-    launches = 1 if args.mode == "persistent" else info["steps"] * info["pieces"]
+    launches = 1 if args.mode == "persistent" else info["launches_per_op"]
     alg_per_launch = info["alg_bytes"] / launches
     launch_sec = sec / launches
     achieved = alg_per_launch / launch_sec / 1e9
@@ -407,7 +410,8 @@ def main():
         "config": {"workload": desc, "nranks": n, "count": count, "input_dtype": dtype,
                    "collective": "reduce-scatter" if coll == "rs" else "all-gather", "exec_mode": args.mode,
                    "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
-                   "pat_steps": info["steps"], "pieces": info["pieces"], "seed": seed},
+                   "pat_steps": info["steps"], "pieces": info["pieces"],
+                   "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"], "seed": seed},
         "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),
         "latency_us": round(ms * 1e3, 2),
         "alg_bytes_per_op": info["alg_bytes"],

@@ -190,6 +190,8 @@ typedef struct {
   size_t slot_bytes_total;    /* all ranks, plus the float32 root accumulators */
   double alg_bytes;           /* memory bytes the steps must read + write per operation */
   double bus_bytes_per_rank;  /* (nranks - 1) * count * sizeof(dtype) */
+  int fused_top_steps;        /* steps run as one fused launch (stream/graph modes, current setting) */
+  int launches_per_op;        /* kernel launches per operation in stream mode (128-bit path if possible) */
 } pat_plan_info_t;
 
 pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,

@@ -87,6 +87,30 @@ int64_t tree_tile_vecs() {
   return 2048;
 }
 
+// Launch-level steps [*s0, *s1) that run as one fused launch, for a plan whose
+// chunk-pieces hold V vectors; empty when nothing is fused.  The top part is
+// the first t steps of the all-gather order and the last t of the
+// reduce-scatter's; AUTO keeps its narrow far end (the reduce-scatter's last
+// steps, the all-gather's first: chunks per rank grow toward the middle).
+void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1, int64_t* tile_vecs) {
+  *s0 = *s1 = 0;
+  *tile_vecs = std::max<int64_t>(1, std::min<int64_t>(V, tree_tile_vecs()));
+  if (fusion == PAT_FUSION_OFF || d.pieces != 1 || d.sched.t < 2) return;
+  const int ns = (int)d.exec.size(), t = d.sched.t;
+  int lo = d.coll == 0 ? 0 : ns - t, hi = d.coll == 0 ? t : ns;
+  if (fusion == PAT_FUSION_AUTO) {
+    const int64_t cap = tree_fuse_vecs();
+    if (d.coll == 1)
+      while (lo < hi && int64_t(d.exec[lo].k) * *tile_vecs > cap) ++lo;
+    else
+      while (hi > lo && int64_t(d.exec[hi - 1].k) * *tile_vecs > cap) --hi;
+  }
+  if (hi - lo >= 2) {
+    *s0 = lo;
+    *s1 = hi;
+  }
+}
+
 uint32_t timeout_us_now() { return g_timeout_us ? g_timeout_us : kDefaultTimeoutUs; }
 
 // Persistent grid: at most this many workgroups per compute unit (0: as many
@@ -146,7 +170,6 @@ struct Plan {
   hipEvent_t upload_done = nullptr;
   bool upload_pending = false;
   hipGraphExec_t graph[2][2][2] = {};  // [vec][own_copy][top part fused]
-  int top_s0 = 0, top_s1 = 0;          // launch-level steps of the top part (empty: not fusable)
   int capacity[pat::kNumVariants][2] = {};
   bool nt_loads = true;
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
@@ -263,13 +286,6 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
   p->nt_loads = nt_loads_for(d.alg_bytes);
   p->alg_bytes = d.alg_bytes;
-  // The top part: the first t steps of the all-gather order, the last t of
-  // the reduce-scatter's (one piece only).
-  if (d.pieces == 1 && d.sched.t >= 2) {
-    const int ns = (int)d.exec.size(), t = d.sched.t;
-    p->top_s0 = coll == 0 ? 0 : ns - t;
-    p->top_s1 = coll == 0 ? t : ns;
-  }
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
@@ -481,25 +497,10 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   } else {
     // Stream and graph modes: one kernel per step, except that the top part
     // may run as one fused launch.
-    const int fusion = fusion_now();
     pat::TreeRange tr{};
-    if (plan->top_s1 > plan->top_s0 && fusion != PAT_FUSION_OFF) {
-      const int64_t V = steps[plan->top_s0].V;
-      tr.s0 = plan->top_s0;
-      tr.s1 = plan->top_s1;
-      tr.tile_vecs = std::min<int64_t>(V, tree_tile_vecs());
-      tr.tiles = (V + tr.tile_vecs - 1) / tr.tile_vecs;
-      if (fusion == PAT_FUSION_AUTO) {
-        // Keep only the narrow far end: the reduce-scatter's last steps, the
-        // all-gather's first (their chunks per rank grow toward the middle).
-        const int64_t cap = tree_fuse_vecs();
-        if (coll == 1)
-          while (tr.s0 < tr.s1 && int64_t(steps[tr.s0].k) * tr.tile_vecs > cap) ++tr.s0;
-        else
-          while (tr.s1 > tr.s0 && int64_t(steps[tr.s1 - 1].k) * tr.tile_vecs > cap) --tr.s1;
-      }
-    }
-    const bool fuse = tr.s1 - tr.s0 >= 2;
+    fused_range(d, steps.empty() ? 0 : steps[0].V, fusion_now(), &tr.s0, &tr.s1, &tr.tile_vecs);
+    const bool fuse = tr.s1 > tr.s0;
+    if (fuse) tr.tiles = (steps[0].V + tr.tile_vecs - 1) / tr.tile_vecs;
     auto enqueue = [&](hipStream_t q) -> hipError_t {
       for (int s = 0; s < (int)steps.size(); ++s) {
         if (fuse && s == tr.s0) {
@@ -653,6 +654,16 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   info.slot_bytes_total = (info.slot_bytes_per_rank + root) * size_t(nranks);
   info.alg_bytes = d.alg_bytes;
   info.bus_bytes_per_rank = double(nranks - 1) * double(count) * d.esize_in;
+  {
+    const pat::Variant var = variant_for((int)coll, dtype, info.vector_path != 0);
+    const int64_t V = int64_t(d.piece_elems) * d.esize_in / pat::variant_in_bytes(var);
+    int s0, s1;
+    int64_t tile;
+    std::lock_guard<std::mutex> lock(g_mu);
+    fused_range(d, V, fusion_now(), &s0, &s1, &tile);
+    info.fused_top_steps = s1 - s0;
+    info.launches_per_op = int(d.exec.size()) * d.pieces - (s1 > s0 ? s1 - s0 - 1 : 0);
+  }
   *out = info;
   return PAT_OK;
 }

@@ -247,3 +247,27 @@ def test_top_fusion_setting_roundtrip():
         assert pat.pat_get_top_fusion() == pat.FUSIONS[m]
     assert pat.pat_set_top_fusion(7) == pat.PAT_ERR_INVALID_ARGUMENT
     assert pat.pat_get_top_fusion() == pat.PAT_FUSION_AUTO
+
+
+@pytest.mark.parametrize("coll", [pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER])
+def test_fused_range_reported_by_plan_info(coll):
+    """Which steps run as one fused launch (stream and graph modes): N=1000
+    with 256-byte chunks fuses the 7 narrow far steps of the top part (16
+    vectors x at most 62 chunks <= 1024), N=6 with 4 KiB chunks its 2 top
+    steps; a top part of one step is never fused."""
+    try:
+        for fusion, want in (("auto", (7, 4)), ("on", (9, 2)), ("off", (0, 10))):
+            pat.check(pat.pat_set_top_fusion(fusion))
+            st, info = pat.pat_plan_info(coll, 1000, 64, "float32")
+            assert st == pat.PAT_OK and info["steps"] == 10 and info["t"] == 9
+            assert (info["fused_top_steps"], info["launches_per_op"]) == want
+        pat.check(pat.pat_set_top_fusion("auto"))
+        st, info = pat.pat_plan_info(coll, 6, 1024, "int32")
+        assert (info["t"], info["fused_top_steps"], info["launches_per_op"]) == (2, 2, 2)
+        # 4 MiB bf16 chunks: the all-gather's slots hold bf16 (T = 2, 64 steps, one top step),
+        # the reduce-scatter's hold float32 partials (T = 1, 127 steps, no top part)
+        st, info = pat.pat_plan_info(coll, 128, 2 << 20, "bfloat16")
+        want = (1, 0, 64) if coll == pat.PAT_ALLGATHER else (0, 0, 127)
+        assert (info["t"], info["fused_top_steps"], info["launches_per_op"]) == want
+    finally:
+        pat.check(pat.pat_set_top_fusion("auto"))
