@@ -65,27 +65,26 @@ int fusion_now() {
   return PAT_FUSION_AUTO;
 }
 
-// PAT_FUSION_AUTO fuses the far end of the top part: the steps whose edges
-// of one tree, times the vectors of one tile, fit this many vectors (about
-// one load round per lane).  Wider steps keep a kernel each, which spreads
-// their edges over the whole chip.  PAT_TREE_FUSE_VECS overrides.
-int64_t tree_fuse_vecs() {
-  if (const char* e = std::getenv("PAT_TREE_FUSE_VECS")) {
+// Vectors of a chunk per workgroup of the fused top part (each tree's chain
+// is sequential inside its workgroup; smaller tiles give more workgroups but
+// measured slower on 64 KiB chunks).  Tuning overrides come from the
+// environment (positive integers only).
+int64_t env_or(const char* name, int64_t dflt) {
+  if (const char* e = std::getenv(name)) {
     const long long v = std::atoll(e);
     if (v > 0) return v;
   }
-  return 1024;
+  return dflt;
 }
+int64_t tree_tile_vecs() { return env_or("PAT_TREE_TILE", 256); }
 
-// Vectors of a chunk per workgroup of the fused top part (PAT_TREE_TILE
-// overrides, for tuning).
-int64_t tree_tile_vecs() {
-  if (const char* e = std::getenv("PAT_TREE_TILE")) {
-    const long long v = std::atoll(e);
-    if (v > 0) return v;
-  }
-  return 2048;
-}
+// PAT_FUSION_AUTO fuses the far end of the top part: the steps that move at
+// most this many bytes (short, latency-bound steps) and whose edges of one
+// tree, times the vectors of one tile, fit about one load round per lane.
+// Larger steps keep a kernel each, which spreads their edges over the whole
+// chip.  PAT_TREE_FUSE_BYTES / PAT_TREE_FUSE_VECS override.
+int64_t tree_fuse_vecs() { return env_or("PAT_TREE_FUSE_VECS", 1024); }
+int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(64) << 20); }
 
 // Launch-level steps [*s0, *s1) that run as one fused launch, for a plan whose
 // chunk-pieces hold V vectors; empty when nothing is fused.  The top part is
@@ -99,11 +98,16 @@ void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1
   const int ns = (int)d.exec.size(), t = d.sched.t;
   int lo = d.coll == 0 ? 0 : ns - t, hi = d.coll == 0 ? t : ns;
   if (fusion == PAT_FUSION_AUTO) {
-    const int64_t cap = tree_fuse_vecs();
+    const int64_t cap = tree_fuse_vecs(), cap_bytes = tree_fuse_bytes();
+    // bytes a step moves: about three chunk transfers per edge
+    auto narrow = [&](int s) {
+      const int64_t k = d.exec[s].k;
+      return k * *tile_vecs <= cap && 3 * int64_t(d.N) * k * d.count * d.esize_in <= cap_bytes;
+    };
     if (d.coll == 1)
-      while (lo < hi && int64_t(d.exec[lo].k) * *tile_vecs > cap) ++lo;
+      while (lo < hi && !narrow(lo)) ++lo;
     else
-      while (hi > lo && int64_t(d.exec[hi - 1].k) * *tile_vecs > cap) --hi;
+      while (hi > lo && !narrow(hi - 1)) --hi;
   }
   if (hi - lo >= 2) {
     *s0 = lo;
