@@ -109,7 +109,14 @@ def cpu_baseline(wid, target_seconds, sample_inputs, m_cap):
         m = int(min(count, m_cap, max(2 * m, m * target_seconds / max(elapsed, 1e-3))))
         elapsed = run(sample_inputs(m))
     bus_bytes = float(n) * (n - 1) * m * esize
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((line.split(":", 1)[1].strip() for line in f if line.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": bus_bytes / elapsed / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "cpu_model": model, "host_cpus_visible": os.cpu_count(),
             "sample": f"all {n} destination chunks x the first {m} of {count} element positions "
                       f"({m / count:.3g} of the operation); numpy, one thread; {elapsed:.1f} s",
             "seconds": round(elapsed, 2)}
@@ -220,6 +227,51 @@ def other_workloads(reps=50):
     return rows
 
 
+def streaming_ceiling(nbytes=4 << 30, reps=10):
+    """The GPU's streaming bandwidth for the step kernels' access shapes, from
+    the plain probe kernels of libpatceiling.so (one 16-byte vector per lane,
+    nontemporal): a copy, and a float32 add of two buffers into a third (the
+    reduce-scatter shape).  GB/s of bytes read + written."""
+    import ctypes
+
+    import torch
+
+    path = os.path.join(ROOT, "paper_2506_20252_amd", "libpatceiling.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    for name, nargs in (("pat_ceiling_copy", 2), ("pat_ceiling_add", 3)):
+        fn = getattr(lib, name)
+        fn.argtypes = [ctypes.c_void_p] * nargs + [ctypes.c_size_t, ctypes.c_void_p]
+        fn.restype = ctypes.c_int
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.full_like(a, 2.0)
+    c = torch.empty_like(a)
+    out = {"bytes_per_buffer": nbytes, "kernel": "16 B/lane, 256 lanes/workgroup, nontemporal"}
+    runs = (("copy_gbps", 2, lambda: lib.pat_ceiling_copy(a.data_ptr(), c.data_ptr(), nbytes, stream.cuda_stream)),
+            ("rs_shape_gbps", 3, lambda: lib.pat_ceiling_add(a.data_ptr(), b.data_ptr(), c.data_ptr(), nbytes,
+                                                             stream.cuda_stream)))
+    for key, streams, op in runs:
+        for _ in range(2):
+            if op() != 0:
+                raise RuntimeError(f"{key}: launch failed")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            op()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out[key] = round(streams * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
+    if not bool(torch.equal(c[:1 << 20], torch.full_like(c[:1 << 20], 3.0))):
+        raise RuntimeError("ceiling probe: wrong sum")
+    del a, b, c
+    torch.cuda.empty_cache()
+    return out
+
+
 def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
     """Time one workload at every aggregation level: the budget is set to the
     bytes of the largest step at T = 1, 2, 4, ... up to full aggregation, so
@@ -317,6 +369,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true", help="skip the small-size latency figures")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-ceiling probes")
     ap.add_argument("--budget-sweep", action="store_true",
                     help="instead: time the workload at every aggregation level (T = 1 .. full)")
     args = ap.parse_args()
@@ -439,6 +492,11 @@ def main():
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds, sample_inputs, min(count, 1 << 20))
     del send, recv, sends, recvs
     torch.cuda.empty_cache()
+    if not args.no_ceiling:
+        ceil = streaming_ceiling()
+        shape_key = "rs_shape_gbps" if coll == "rs" else "copy_gbps"
+        ceil["roofline_achieved_over_" + shape_key] = round(achieved / ceil[shape_key], 4)
+        out["streaming_ceiling"] = ceil
     print(json.dumps(out), flush=True)
 
 

@@ -2,6 +2,8 @@
 
 * paper_2506_20252_amd/libpat.so -- the PAT collectives (C-ABI of include/pat.h)
 * synth/libpatsynth.so           -- the seeded input filler used by tests and the benchmark
+* paper_2506_20252_amd/libpatceiling.so -- streaming-ceiling probes (copy, 2-read/1-write add) that
+                                          the benchmark reports beside the collectives
 """
 
 import os
@@ -19,6 +21,7 @@ TARGETS = [
     (os.path.join(PKG, "libpat.so"),
      [os.path.join(CSRC, f) for f in ("plan.cpp", "api.cpp", "kernels.hip")]),
     (os.path.join(ROOT, "synth", "libpatsynth.so"), [os.path.join(ROOT, "synth", "synth.hip")]),
+    (os.path.join(PKG, "libpatceiling.so"), [os.path.join(CSRC, "ceiling.hip")]),
 ]
 
 
