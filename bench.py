@@ -54,11 +54,38 @@ KERNEL_SOURCES = ["paper_2506_20252_amd/csrc/kernels.hip", "paper_2506_20252_amd
                   "paper_2506_20252_amd/csrc/device_types.hpp"]
 
 
+def _code_only(text):
+    """C/C++ source without comments and whitespace: what the compiler sees
+    (string and character literals kept intact)."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        ch = text[i]
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        elif ch in "\"'":
+            j = i + 1
+            while j < n and text[j] != ch:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            if not ch.isspace():
+                out.append(ch)
+            i += 1
+    return "".join(out)
+
+
 def kernel_source_hash():
+    """Hash of the kernel sources' code (comments and whitespace ignored), so
+    that counter summaries stay valid across comment edits only."""
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel)) as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

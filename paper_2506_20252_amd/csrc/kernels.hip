@@ -6,11 +6,13 @@
 //           addresses computed once per workgroup (wavefront-uniform);
 //   packed: chunks smaller than a tile; consecutive vectors of consecutive
 //           edges, addresses computed per lane.
-// Every lane issues all of its loads before any store: kUnroll vectors per
-// stream, 16 bytes each (bf16 reduce-scatter: 8-byte inputs beside 16-byte
-// float32 partials, at twice the unroll).  Accesses use explicit global
-// pointers, stores are nontemporal, and loads are nontemporal for operations
-// far larger than the Infinity Cache.  The data path has no matrix work and no
+// Every lane issues all of its loads before it uses any (U vectors per
+// stream, 16 bytes each; bf16 reduce-scatter: 8-byte inputs beside 16-byte
+// float32 partials, at twice the unroll) and stores only after every value of
+// its tile is computed, so that neither a conversion nor a store in a branch
+// makes the compiler wait for one access before the next.  Accesses use
+// explicit global pointers, stores are nontemporal, and loads are nontemporal
+// for operations far larger than the Infinity Cache.  The data path has no matrix work and no
 // reuse, so there is no LDS staging: a load lands in VGPRs and is stored from
 // there.
 //
@@ -33,7 +35,8 @@
 // at step s + 1).  Per-step launches get the ordering from the kernel
 // boundary; the persistent kernel orders its work queue by per-step
 // completion counters whose fences make every workgroup's writes visible
-// across the XCDs' separate L2 caches.
+// across the XCDs' separate L2 caches; the fused top part (tree_kernel) needs
+// only workgroup barriers, since there each tree's data is its workgroup's.
 
 #include <hip/hip_runtime.h>
 
