@@ -131,14 +131,15 @@ int blocks_per_cu_cap(double bytes_per_step) {
   return 0;
 }
 
-// Loads stream (nontemporal) when an operation moves at least this many bytes;
-// smaller operations keep their data in the 256 MB Infinity Cache between
-// steps.  PAT_NT_LOADS=0/1 overrides.
-constexpr double kStreamingLoadBytes = 1e9;
+// Loads and stores stream (nontemporal) when an operation moves at least this
+// many bytes; smaller operations keep their data in the 256 MB Infinity Cache
+// between steps (measured on MI355X: plain accesses are 6-17% faster below,
+// streaming ones 8-12% faster far above).  PAT_STREAMING=0/1 overrides.
+constexpr double kStreamingBytes = 1e9;
 
-bool nt_loads_for(double alg_bytes) {
-  if (const char* e = std::getenv("PAT_NT_LOADS")) return e[0] == '1';
-  return alg_bytes >= kStreamingLoadBytes;
+bool streaming_for(double alg_bytes) {
+  if (const char* e = std::getenv("PAT_STREAMING")) return e[0] == '1';
+  return alg_bytes >= kStreamingBytes;
 }
 
 int elem_size(pat_dtype_t t) { return t == PAT_BFLOAT16 ? 2 : 4; }
@@ -175,7 +176,7 @@ struct Plan {
   bool upload_pending = false;
   hipGraphExec_t graph[2][2][2] = {};  // [vec][own_copy][top part fused]
   int capacity[pat::kNumVariants][2] = {};
-  bool nt_loads = true;
+  bool streaming = true;
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
   int cus = 0;
   int64_t clock_khz = 0;
@@ -288,7 +289,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   const pat::Variant vs = variant_for(coll, dt, false), vv = variant_for(coll, dt, true);
   if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
-  p->nt_loads = nt_loads_for(d.alg_bytes);
+  p->streaming = streaming_for(d.alg_bytes);
   p->alg_bytes = d.alg_bytes;
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
@@ -350,10 +351,10 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
     if (e[0] == '1') {
       std::fprintf(stderr,
                    "[pat] plan coll=%d N=%d count=%lld dtype=%d L=%d t=%d T=%d steps=%zu pieces=%d "
-                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d nt_loads=%d\n",
+                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d streaming=%d\n",
                    coll, N, (long long)count, (int)dt, d.sched.L, d.sched.t, d.sched.T, d.exec.size(),
                    d.pieces, d.max_k, d.slots.entries, (long long)(p->slot_rank_stride * N), d.alg_bytes,
-                   (int)p->has_vec, (int)p->nt_loads);
+                   (int)p->has_vec, (int)p->streaming);
     }
   }
   *out = p.get();
@@ -484,7 +485,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   const auto& steps = plan->steps[vi];
   const int mode = mode_now();
   if (mode == PAT_EXEC_PERSISTENT) {
-    const bool nt = plan->nt_loads;
+    const bool nt = plan->streaming;
     int& capacity = plan->capacity[var][nt ? 1 : 0];
     if (capacity == 0) HIP_TRY(pat::persistent_capacity(var, nt, &capacity));
     int64_t most = 1;
@@ -508,12 +509,12 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     auto enqueue = [&](hipStream_t q) -> hipError_t {
       for (int s = 0; s < (int)steps.size(); ++s) {
         if (fuse && s == tr.s0) {
-          const hipError_t e = pat::launch_tree(var, plan->nt_loads, cx, tr, q);
+          const hipError_t e = pat::launch_tree(var, plan->streaming, cx, tr, q);
           if (e != hipSuccess) return e;
           s = tr.s1 - 1;
           continue;
         }
-        const hipError_t e = pat::launch_step(var, plan->nt_loads, cx, steps[s], q);
+        const hipError_t e = pat::launch_step(var, plan->streaming, cx, steps[s], q);
         if (e != hipSuccess) return e;
       }
       return hipSuccess;

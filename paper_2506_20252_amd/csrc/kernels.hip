@@ -11,8 +11,9 @@
 // float32 partials, at twice the unroll) and stores only after every value of
 // its tile is computed, so that neither a conversion nor a store in a branch
 // makes the compiler wait for one access before the next.  Accesses use
-// explicit global pointers, stores are nontemporal, and loads are nontemporal
-// for operations far larger than the Infinity Cache.  The data path has no matrix work and no
+// explicit global pointers; loads and stores are nontemporal for operations
+// far larger than the Infinity Cache, and plain (cached) otherwise, so that a
+// small operation's next step finds the slots just written still in cache.  The data path has no matrix work and no
 // reuse, so there is no LDS staging: a load lands in VGPRs and is stored from
 // there.
 //
@@ -44,18 +45,15 @@
 
 #include "kernels.hpp"
 
-// Tuning knobs (compile time): vectors in flight per lane, nontemporal
-// (streaming) stores, and the XCD-aware work-item order.
+// Tuning knobs (compile time): vectors in flight per lane and the XCD-aware
+// work-item order.  Whether loads and stores stream (nontemporal) is a launch
+// argument, chosen per plan.
 #ifndef PAT_UNROLL
 #define PAT_UNROLL 2
 #endif
 // bf16 reduce-scatter: 8-byte input vectors beside 16-byte float32 partials.
 #ifndef PAT_B16_UNROLL
 #define PAT_B16_UNROLL (2 * PAT_UNROLL)
-#endif
-// Stores always stream; the loads' hint is chosen per plan (launch argument).
-#ifndef PAT_NT_STORES
-#define PAT_NT_STORES 1
 #endif
 // 1: workgroup b of a step takes work item (b % 8) * ceil(items / 8) + b / 8,
 // so that consecutive tiles (contiguous memory) run on one XCD (workgroups are
@@ -85,10 +83,10 @@ __device__ __forceinline__ T ldg(const char* p) {
   return *q;
 }
 
-template <typename T>
+template <bool NT, typename T>
 __device__ __forceinline__ void stg(char* p, const T& v) {
   PAT_GLOBAL T* q = (PAT_GLOBAL T*)(p);
-  if constexpr (PAT_NT_STORES)
+  if constexpr (NT)
     __builtin_nontemporal_store(v, q);
   else
     *q = v;
@@ -165,7 +163,7 @@ __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st
 // All-gather
 // ---------------------------------------------------------------------------
 
-template <typename Unit, int kU, bool NTL>
+template <typename Unit, int kU, bool NT>
 struct AgOp {
   static constexpr int U = kU;
   static constexpr int kTile = kThreads * U;
@@ -201,9 +199,9 @@ struct AgOp {
 
   __device__ static void put(const Edge& e, int64_t v, const Unit& x) {
     const int64_t o = v * (int64_t)sizeof(Unit);
-    stg(e.dst + o, x);
-    if (e.dst2) stg(e.dst2 + o, x);
-    if (e.dst3) stg(e.dst3 + o, x);
+    stg<NT>(e.dst + o, x);
+    if (e.dst2) stg<NT>(e.dst2 + o, x);
+    if (e.dst3) stg<NT>(e.dst3 + o, x);
   }
 
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
@@ -218,23 +216,23 @@ struct AgOp {
         // Full tile (uniform): straight-line loads, then one store loop per
         // destination, so no store waits for another store.
 #pragma unroll
-        for (int j = 0; j < U; ++j) x[j] = ldg<Unit, NTL>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
+        for (int j = 0; j < U; ++j) x[j] = ldg<Unit, NT>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         if (e.dst2) {
 #pragma unroll
-          for (int j = 0; j < U; ++j) stg(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < U; ++j) stg<NT>(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         if (e.dst3) {
 #pragma unroll
-          for (int j = 0; j < U; ++j) stg(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < U; ++j) stg<NT>(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         return;
       }
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t v = v0 + j * kThreads;
-        if (v < st.V) x[j] = ldg<Unit, NTL>(e.src + v * (int64_t)sizeof(Unit));
+        if (v < st.V) x[j] = ldg<Unit, NT>(e.src + v * (int64_t)sizeof(Unit));
       }
       wait_loads();
 #pragma unroll
@@ -276,7 +274,7 @@ struct AgOp {
       if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) x[j] = ldg<Unit, NTL>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+      if (vv[j] >= 0) x[j] = ldg<Unit, NT>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
@@ -373,7 +371,7 @@ struct TB16S {
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
 };
 
-template <class R, bool NTL>
+template <class R, bool NT>
 struct RsOp {
   using in_t = typename R::in_t;
   using acc_t = typename R::acc_t;
@@ -430,9 +428,9 @@ struct RsOp {
 
   __device__ static void store(const Edge& e, int64_t v, const acc_t& x) {
     if (e.dst_final)
-      stg(e.dst + v * (int64_t)sizeof(in_t), R::narrow(x));
+      stg<NT>(e.dst + v * (int64_t)sizeof(in_t), R::narrow(x));
     else
-      stg(e.dst + v * (int64_t)sizeof(acc_t), x);
+      stg<NT>(e.dst + v * (int64_t)sizeof(acc_t), x);
   }
 
   // One tile of one edge whose operand kinds are known: every load is issued
@@ -448,18 +446,18 @@ struct RsOp {
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const int64_t v = v0 + j * kThreads;
-        a[j] = ldg<vec_t<OWN_RAW>, NTL>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
-        b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+        a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
+        b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
       acc_t sum[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
       if (R::kSeparateRoot && e.dst_final) {
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
+        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
       } else {
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
+        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
       }
       return;
     }
@@ -467,8 +465,8 @@ struct RsOp {
     for (int j = 0; j < U; ++j) {
       const int64_t v = v0 + j * kThreads;
       if (v < V) {
-        a[j] = ldg<vec_t<OWN_RAW>, NTL>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
-        b[j] = ldg<vec_t<CHILD_RAW>, NTL>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+        a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
+        b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
     }
     acc_t sum[U];
@@ -540,17 +538,17 @@ struct RsOp {
     for (int j = 0; j < U; ++j) {
       if (vv[j] >= 0) {
         if constexpr (kSameVec) {
-          xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
-          xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+          xa[j] = ldg<acc_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+          xb[j] = ldg<acc_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
         } else {
           if (e[j].own_in)
-            ra[j] = ldg<in_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
+            ra[j] = ldg<in_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
           else
-            xa[j] = ldg<acc_t, NTL>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+            xa[j] = ldg<acc_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
           if (e[j].child_in)
-            rb[j] = ldg<in_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
+            rb[j] = ldg<in_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
           else
-            xb[j] = ldg<acc_t, NTL>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+            xb[j] = ldg<acc_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
         }
       }
     }
@@ -871,9 +869,9 @@ int variant_tile(Variant v) {
 
 #define PAT_UNPAREN(...) __VA_ARGS__
 
-hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream) {
+hipError_t launch_step(Variant v, bool streaming, const KCtx& cx, const DevStep& st, hipStream_t stream) {
 #define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, stream)
-  PAT_DISPATCH(v, nt_loads, PAT_STEP)
+  PAT_DISPATCH(v, streaming, PAT_STEP)
 #undef PAT_STEP
 }
 
@@ -886,21 +884,21 @@ hipError_t launch_tree_t(const KCtx& cx, const TreeRange& tr, hipStream_t stream
   return hipGetLastError();
 }
 
-hipError_t launch_tree(Variant v, bool nt_loads, const KCtx& cx, const TreeRange& tr, hipStream_t stream) {
+hipError_t launch_tree(Variant v, bool streaming, const KCtx& cx, const TreeRange& tr, hipStream_t stream) {
 #define PAT_TREE(OP) launch_tree_t<PAT_UNPAREN OP>(cx, tr, stream)
-  PAT_DISPATCH(v, nt_loads, PAT_TREE)
+  PAT_DISPATCH(v, streaming, PAT_TREE)
 #undef PAT_TREE
 }
 
-hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream) {
+hipError_t launch_persistent(Variant v, bool streaming, const KCtx& cx, int grid, hipStream_t stream) {
 #define PAT_PERS(OP) launch_persistent_t<PAT_UNPAREN OP>(cx, grid, stream)
-  PAT_DISPATCH(v, nt_loads, PAT_PERS)
+  PAT_DISPATCH(v, streaming, PAT_PERS)
 #undef PAT_PERS
 }
 
-hipError_t persistent_capacity(Variant v, bool nt_loads, int* blocks) {
+hipError_t persistent_capacity(Variant v, bool streaming, int* blocks) {
 #define PAT_CAP(OP) capacity_t<PAT_UNPAREN OP>(blocks)
-  PAT_DISPATCH(v, nt_loads, PAT_CAP)
+  PAT_DISPATCH(v, streaming, PAT_CAP)
 #undef PAT_CAP
 }
 

@@ -58,9 +58,10 @@ enum Variant : int {
 int variant_in_bytes(Variant v);
 int variant_tile(Variant v);
 
-// nt_loads: nontemporal (streaming) loads, for operations much larger than the
-// 256 MB Infinity Cache; plain loads let small operations hit in it.
-hipError_t launch_step(Variant v, bool nt_loads, const KCtx& cx, const DevStep& st, hipStream_t stream);
+// streaming: nontemporal loads and stores, for operations much larger than
+// the 256 MB Infinity Cache; plain accesses let a small operation's steps
+// hit in it (each step reads the slots the previous one wrote).
+hipError_t launch_step(Variant v, bool streaming, const KCtx& cx, const DevStep& st, hipStream_t stream);
 // Fused top part: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
 struct TreeRange {
@@ -68,12 +69,12 @@ struct TreeRange {
   int64_t tile_vecs;
   int64_t tiles;
 };
-hipError_t launch_tree(Variant v, bool nt_loads, const KCtx& cx, const TreeRange& tr, hipStream_t stream);
+hipError_t launch_tree(Variant v, bool streaming, const KCtx& cx, const TreeRange& tr, hipStream_t stream);
 // Persistent execution: one launch of `grid` workgroups that take per-step
 // worker ids from device counters in step order.  Any grid size is safe (a
 // workgroup only waits on work that running workgroups already hold).
-hipError_t launch_persistent(Variant v, bool nt_loads, const KCtx& cx, int grid, hipStream_t stream);
+hipError_t launch_persistent(Variant v, bool streaming, const KCtx& cx, int grid, hipStream_t stream);
 // Workgroups of the persistent kernel that fit on the current device at once.
-hipError_t persistent_capacity(Variant v, bool nt_loads, int* blocks);
+hipError_t persistent_capacity(Variant v, bool streaming, int* blocks);
 
 }  // namespace pat
