@@ -157,7 +157,7 @@ int pat_get_exec_mode(void);
  * chunks per rank) are better left to one kernel each.  AUTO (the default, or
  * the PAT_TOP_FUSION environment variable: auto | on | off) fuses the far end
  * of the top part, the steps that move at most 64 MiB and in which one tree's
- * edges over one tile of its chunk (256 vectors) amount to at most 1024
+ * edges over one tile of its chunk (256 vectors) amount to at most 2048
  * vectors, when there are two or more such steps;
  * ON fuses the whole top part whenever it has two or more steps.  Neither
  * fuses a chunk that is split into pieces.

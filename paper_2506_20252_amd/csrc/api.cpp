@@ -80,10 +80,10 @@ int64_t tree_tile_vecs() { return env_or("PAT_TREE_TILE", 256); }
 
 // PAT_FUSION_AUTO fuses the far end of the top part: the steps that move at
 // most this many bytes (short, latency-bound steps) and whose edges of one
-// tree, times the vectors of one tile, fit about one load round per lane.
+// tree, times the vectors of one tile, fit a few load rounds per lane.
 // Larger steps keep a kernel each, which spreads their edges over the whole
 // chip.  PAT_TREE_FUSE_BYTES / PAT_TREE_FUSE_VECS override.
-int64_t tree_fuse_vecs() { return env_or("PAT_TREE_FUSE_VECS", 1024); }
+int64_t tree_fuse_vecs() { return env_or("PAT_TREE_FUSE_VECS", 2048); }
 int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(64) << 20); }
 
 // Launch-level steps [*s0, *s1) that run as one fused launch, for a plan whose
