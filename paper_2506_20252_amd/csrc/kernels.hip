@@ -133,6 +133,15 @@ __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int*
   *i = (int)(e - (int64_t)(*r) * st.k);
 }
 
+// Workgroup size of the fused top part.  A tree's steps run one after another
+// inside its workgroup, so a wide workgroup covers a whole step in fewer load
+// rounds (a shorter chain of dependent accesses per step).
+#ifndef PAT_TREE_THREADS
+#define PAT_TREE_THREADS 256
+#endif
+constexpr int kTreeThreads = PAT_TREE_THREADS;
+static_assert(kTreeThreads % 64 == 0 && kTreeThreads <= 1024, "tree workgroup: whole wavefronts, at most 1024 lanes");
+
 // One step of one tree in a fused top part: the pairs (entry i, vector v)
 // with i < k and v in [t0, t0 + TV), flattened vector-fastest so that lanes
 // sweep each edge's tile contiguously, U pairs per lane at a time.
@@ -140,12 +149,12 @@ template <class Op>
 __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
   constexpr int U = Op::U;
   const int64_t n = (int64_t)st.k * TV;
-  for (int64_t base = 0; base < n; base += (int64_t)kThreads * U) {
+  for (int64_t base = 0; base < n; base += (int64_t)kTreeThreads * U) {
     int rr[U], ii[U];
     int64_t vv[U];
 #pragma unroll
     for (int j = 0; j < U; ++j) {
-      const int64_t f = base + j * kThreads + threadIdx.x;
+      const int64_t f = base + j * kTreeThreads + threadIdx.x;
       vv[j] = -1;
       rr[j] = c;
       ii[j] = 0;
@@ -599,7 +608,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
 // A workgroup barrier between steps then replaces the kernel boundary; each
 // wave first waits for its own stores.
 template <class Op>
-__global__ __launch_bounds__(kThreads) void tree_kernel(KCtx cx, TreeRange tr) {
+__global__ __launch_bounds__(kTreeThreads) void tree_kernel(KCtx cx, TreeRange tr) {
   const int c = (int)(blockIdx.x / tr.tiles);
   const int64_t tile = (int64_t)blockIdx.x - (int64_t)c * tr.tiles;
   const int64_t t0 = tile * tr.tile_vecs;
@@ -880,7 +889,7 @@ hipError_t launch_tree_t(const KCtx& cx, const TreeRange& tr, hipStream_t stream
   const int64_t grid = (int64_t)cx.N * tr.tiles;
   if (tr.s1 <= tr.s0 || grid <= 0) return hipSuccess;
   if (grid >= (int64_t(1) << 31) || tr.tile_vecs <= 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(tree_kernel<Op>, dim3((unsigned)grid), dim3(kThreads), 0, stream, cx, tr);
+  hipLaunchKernelGGL(tree_kernel<Op>, dim3((unsigned)grid), dim3(kTreeThreads), 0, stream, cx, tr);
   return hipGetLastError();
 }
 
