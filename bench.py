@@ -491,7 +491,8 @@ def main():
                    "collective": "reduce-scatter" if coll == "rs" else "all-gather", "exec_mode": args.mode,
                    "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
                    "pat_steps": info["steps"], "pieces": info["pieces"],
-                   "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"], "seed": seed},
+                   "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"],
+                   "streaming_accesses": bool(info["streaming"]), "seed": seed},
         "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),
         "latency_us": round(ms * 1e3, 2),
         "alg_bytes_per_op": info["alg_bytes"],

@@ -669,6 +669,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
     info.fused_top_steps = s1 - s0;
     info.launches_per_op = int(d.exec.size()) * d.pieces - (s1 > s0 ? s1 - s0 - 1 : 0);
   }
+  info.streaming = streaming_for(d.alg_bytes) ? 1 : 0;
   *out = info;
   return PAT_OK;
 }

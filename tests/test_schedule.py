@@ -271,3 +271,21 @@ def test_fused_range_reported_by_plan_info(coll):
         assert (info["t"], info["fused_top_steps"], info["launches_per_op"]) == want
     finally:
         pat.check(pat.pat_set_top_fusion("auto"))
+
+
+def test_streaming_choice_reported_by_plan_info(monkeypatch):
+    """Operations of >= 1e9 algorithmic bytes stream (nontemporal accesses);
+    smaller ones keep their slots cached between steps; PAT_STREAMING forces
+    either."""
+    for args, want in (((pat.PAT_REDUCESCATTER, 128, 2 << 20, "bfloat16"), 1),
+                       ((pat.PAT_REDUCESCATTER, 64, 262144, "float32"), 1),
+                       ((pat.PAT_REDUCESCATTER, 1000, 64, "float32"), 0),
+                       ((pat.PAT_ALLGATHER, 24, 32768, "bfloat16"), 0)):
+        st, info = pat.pat_plan_info(*args)
+        assert st == pat.PAT_OK
+        assert info["streaming"] == want, args
+        assert (info["alg_bytes"] >= 1e9) == bool(want)
+    monkeypatch.setenv("PAT_STREAMING", "1")
+    assert pat.pat_plan_info(pat.PAT_ALLGATHER, 24, 32768, "bfloat16")[1]["streaming"] == 1
+    monkeypatch.setenv("PAT_STREAMING", "0")
+    assert pat.pat_plan_info(pat.PAT_REDUCESCATTER, 64, 262144, "float32")[1]["streaming"] == 0
