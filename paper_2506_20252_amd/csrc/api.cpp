@@ -174,7 +174,9 @@ struct Plan {
   void** pinned = nullptr;  // 2N pointers staged for upload
   hipEvent_t upload_done = nullptr;
   bool upload_pending = false;
-  hipGraphExec_t graph[2][2][2] = {};  // [vec][own_copy][top part fused]
+  // Captured graphs by [vec][own_copy] and fused step range (s0, s1): a
+  // change of the fusion setting selects or captures its own graph.
+  std::map<std::tuple<int, int, int, int>, hipGraphExec_t> graphs;
   int capacity[pat::kNumVariants][2] = {};
   bool streaming = true;
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
@@ -186,10 +188,8 @@ struct Plan {
   uint64_t last_use = 0;     // LRU stamp
 
   ~Plan() {
-    for (auto& plane : graph)
-      for (auto& row : plane)
-        for (auto& g : row)
-          if (g) (void)hipGraphExecDestroy(g);
+    for (auto& kv : graphs)
+      if (kv.second) (void)hipGraphExecDestroy(kv.second);
     if (done) (void)hipEventDestroy(done);
     if (upload_done) (void)hipEventDestroy(upload_done);
     if (pinned) (void)hipHostFree(pinned);
@@ -522,7 +522,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     if (mode == PAT_EXEC_STREAM) {
       HIP_TRY(enqueue(stream));
     } else {
-      hipGraphExec_t& exec = plan->graph[vi][cx.own_copy][fuse ? 1 : 0];
+      hipGraphExec_t& exec = plan->graphs[std::make_tuple(vi, cx.own_copy, tr.s0, tr.s1)];
       if (!exec) {
         hipStream_t cs = nullptr;
         HIP_TRY(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
