@@ -450,3 +450,69 @@ def test_graph_mode_follows_fusion_changes_on_one_plan():
     exact = D.reducescatter_sum(dev_in, "float32")
     scale = D.reducescatter_abs_sum(dev_in, "float32")
     assert (np.abs(outs[0].astype(np.float64) - exact) <= 1e-5 * scale).all()
+
+
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+def test_caller_created_stream(mode):
+    """The collectives run on the stream they are given, not only on the
+    default one."""
+    n, count, seed = 13, 3000, 0x57E
+    dev = torch.device("cuda:0")
+    send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+    fill_ranks(send, "f32_normal", seed)
+    recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+    agin = torch.empty((n, count), dtype=torch.bfloat16, device=dev)
+    fill_ranks(agin, "bf16_normal", seed + 1)
+    agout = torch.empty((n, n * count), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream(device=dev)  # default priority
+    pat.check(pat.pat_set_exec_mode(mode))
+    log(f"[gpu] caller stream, mode={mode}")
+    pat.check(pat.pat_reducescatter(list(send), list(recv), count, "float32", pat.PAT_SUM, n, side))
+    pat.check(pat.pat_allgather(list(agin), list(agout), count, "bfloat16", n, side))
+    pat.check(pat.pat_check_device_status(side))
+    check_rs(as_bits(recv), host_rs_inputs(n, count, "f32_normal", seed), "float32",
+             oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
+    host_in = np.stack([synth.host_buffer("bf16_normal", seed + 1, x, count) for x in range(n)])
+    np.testing.assert_array_equal(as_bits(agout).reshape(n, n, count), D.allgather(host_in))
+
+
+def test_two_host_threads_on_their_own_streams():
+    """Two host threads issue collectives concurrently, each on its own stream
+    and plan; the library serialises its host-side work and the device runs
+    both streams at once."""
+    import threading
+
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode("stream"))
+    jobs = [(9, 4000, 0x7A1), (17, 2500, 0x7A2)]
+    bufs = []
+    for n, count, seed in jobs:
+        send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+        fill_ranks(send, "f32_normal", seed)
+        bufs.append((send, torch.empty((n, count), dtype=torch.float32, device=dev)))
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(idx):
+        try:
+            n, count, _ = jobs[idx]
+            send, recv = bufs[idx]
+            s = torch.cuda.Stream(device=dev)
+            S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+            for _ in range(20):
+                pat.check(pat.pat_reducescatter(S, R, count, "float32", pat.PAT_SUM, n, s))
+            pat.check(pat.pat_check_device_status(s))
+        except Exception as exc:  # reported by the main thread
+            errors.append(exc)
+
+    log("[gpu] two host threads")
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for (n, count, seed), (send, recv) in zip(jobs, bufs):
+        check_rs(as_bits(recv), host_rs_inputs(n, count, "f32_normal", seed), "float32",
+                 oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
