@@ -48,6 +48,9 @@ WORKLOADS = {
     5: ("rs", 128, 2097152, "bfloat16", "bf16_normal", 0x5041545,
         "PAT reduce-scatter (sum), N=128 virtual ranks, bf16 N(0,1) in / fp32 accumulation, "
         "2097152-element (4 MiB) output chunk per rank, 64 GiB of rank buffers in HBM"),
+    # the all-gather of the small-size regime (workload 4's other collective)
+    6: ("ag", 1000, 64, "float32", "f32_pm1", 0x5041544,
+        "PAT all-gather, N=1000 virtual ranks, fp32 U[-1,1), 64-element (256 B) chunk per rank"),
 }
 
 KERNEL_SOURCES = ["paper_2506_20252_amd/csrc/kernels.hip", "paper_2506_20252_amd/csrc/kernels.hpp",
