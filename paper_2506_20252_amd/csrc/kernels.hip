@@ -119,7 +119,7 @@ __device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r,
   }
 }
 
-// Waits for every outstanding memory access of this lane.  Used between a
+// Waits for every outstanding memory access of this wave.  Used between a
 // load phase and stores that sit in per-lane branches: there the compiler
 // cannot count which loads a store still needs and waits before each store
 // for all earlier ones, stores included; one wait up front avoids that.
@@ -634,7 +634,7 @@ __global__ __launch_bounds__(kTreeThreads) void tree_kernel(KCtx cx, TreeRange t
 // No co-residency is needed: a workgroup enters step s only after every id of
 // step s - 1 was taken by a running workgroup, and those depend only on
 // earlier steps, so by induction over the steps all work completes whatever
-// the grid size.  The launch is a plain one, at full occupancy.
+// the grid size.  The launch is a plain one; the host sizes its grid.
 //
 // Counters are spread over kShards cache lines per step: atomics on a single
 // address serialise (about 11 ns each on MI355X, 20 us for one round of 1792
