@@ -516,3 +516,21 @@ def test_two_host_threads_on_their_own_streams():
     for (n, count, seed), (send, recv) in zip(jobs, bufs):
         check_rs(as_bits(recv), host_rs_inputs(n, count, "f32_normal", seed), "float32",
                  oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
+
+
+def test_large_rank_count_n2049():
+    """N = 2049 (L = 12, not a power of two), full aggregation, tiny chunks:
+    int32 and float32 reduce-scatter and all-gather on the 128-bit path
+    (4 elements) and the element path (3 elements), every output checked."""
+    n = 2049
+    got = run_rs(n, 4, "int32", 0x801, mode="stream")
+    np.testing.assert_array_equal(got, D.reducescatter_sum(host_rs_inputs(n, 4, "int32_pm2p20", 0x801), "int32"))
+    got = run_rs(n, 3, "float32", 0x802, mode="stream")
+    host_in = host_rs_inputs(n, 3, "f32_normal", 0x802)
+    exact = D.reducescatter_sum(host_in, "float32")
+    scale = D.reducescatter_abs_sum(host_in, "float32")
+    assert (np.abs(got.astype(np.float64) - exact) <= 1e-5 * scale).all()
+    for count, dtype in ((3, "float32"), (8, "bfloat16")):
+        got, host_in = run_ag(n, count, dtype, 0x803 + count, mode="stream")
+        np.testing.assert_array_equal(got, D.allgather(host_in))
+    torch.cuda.empty_cache()

@@ -289,3 +289,21 @@ def test_streaming_choice_reported_by_plan_info(monkeypatch):
     assert pat.pat_plan_info(pat.PAT_ALLGATHER, 24, 32768, "bfloat16")[1]["streaming"] == 1
     monkeypatch.setenv("PAT_STREAMING", "0")
     assert pat.pat_plan_info(pat.PAT_REDUCESCATTER, 64, 262144, "float32")[1]["streaming"] == 0
+
+
+@pytest.mark.parametrize("n", [2048, 4096, 4097])
+def test_large_rank_counts_match_oracle(n):
+    """Large N at full aggregation and at T = 1 (the two ends of the budget
+    range): the library's steps equal the oracle's, ceil(log2 N) and N - 1."""
+    count = 4
+    L = opat.ceil_log2(n)
+    try:
+        for t in (L - 1, 0):
+            pat.pat_set_buffer_bytes(budget_for(n, t, count * 4))
+            for coll, rev in ((pat.PAT_ALLGATHER, False), (pat.PAT_REDUCESCATTER, True)):
+                got, steps, _ = library_steps(coll, n, count, "float32")
+                ref = [(d, sorted(P)) for d, P in opat.schedule(n, t)]
+                assert got == (ref[::-1] if rev else ref)
+                assert len(steps) == (L if t == L - 1 else n - 1)
+    finally:
+        pat.pat_set_buffer_bytes(0)
