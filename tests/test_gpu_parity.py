@@ -534,3 +534,22 @@ def test_large_rank_count_n2049():
         got, host_in = run_ag(n, count, dtype, 0x803 + count, mode="stream")
         np.testing.assert_array_equal(got, D.allgather(host_in))
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("tile", ["7", "100"])
+def test_top_fusion_with_odd_tiles(tile, monkeypatch):
+    """The fused kernel with tiles that do not divide the chunk: many tiles
+    per tree and a ragged last one, every dtype, both collectives."""
+    monkeypatch.setenv("PAT_TREE_TILE", tile)
+    pat.check(pat.pat_set_top_fusion("on"))
+    try:
+        for n, count in ((13, 1000), (33, 4104)):
+            for dtype in ("int32", "float32", "bfloat16"):
+                seed = 41 * n + count + int(tile)
+                got, host_in = run_ag(n, count, dtype, seed, mode="stream")
+                np.testing.assert_array_equal(got, D.allgather(host_in))
+                got = run_rs(n, count, dtype, seed + 1, mode="stream")
+                check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+                         oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+    finally:
+        pat.check(pat.pat_set_top_fusion("auto"))
