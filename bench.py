@@ -367,6 +367,67 @@ def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
                       "nranks": n, "log2_n": round(math.log2(n), 3), "rows": rows}), flush=True)
 
 
+def size_sweep(n=128, max_input_bytes=16 << 30, reps_bytes=32 << 30):
+    """Both collectives at one rank count over chunk sizes from 256 B up, at
+    the default budget: microseconds per operation, steps and launches, bus
+    bandwidth and the fraction of HBM peak that the algorithmic bytes reach --
+    where the latency regime ends and the bandwidth roofline begins.  float32
+    reduce-scatter and all-gather, N(0,1) inputs, seed 0x5153."""
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for coll in ("rs", "ag"):
+        count = 64  # 256 B
+        while n * n * count * 4 <= max_input_bytes:
+            if coll == "rs":
+                send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+                recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+                code = pat.PAT_REDUCESCATTER
+            else:
+                send = torch.empty((n, count), dtype=torch.float32, device=dev)
+                recv = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+                code = pat.PAT_ALLGATHER
+            for x in range(n):
+                synth.fill(send[x], "f32_normal", 0x5153, x)
+            S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+
+            def op():
+                if coll == "rs":
+                    return pat.pat_reducescatter(S, R, count, "float32", pat.PAT_SUM, n, stream)
+                return pat.pat_allgather(S, R, count, "float32", n, stream)
+
+            st, info = pat.pat_plan_info(code, n, count, "float32")
+            reps = int(max(5, min(200, reps_bytes / max(info["alg_bytes"], 1.0))))
+            for _ in range(3):
+                pat.check(op())
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(reps):
+                pat.check(op())
+            e1.record(stream)
+            torch.cuda.synchronize()
+            pat.check(pat.pat_check_device_status(stream))
+            sec = e0.elapsed_time(e1) / 1e3 / reps
+            rows.append({"collective": "reduce-scatter" if coll == "rs" else "all-gather", "chunk_bytes": count * 4,
+                         "T": info["T"], "steps": info["steps"], "launches": info["launches_per_op"],
+                         "streaming": bool(info["streaming"]), "us": round(sec * 1e6, 2),
+                         "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 1),
+                         "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
+            print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+            del send, recv, S, R
+            pat.check(pat.pat_finalize())
+            torch.cuda.empty_cache()
+            count *= 4
+    print(json.dumps({"metric": "PAT size sweep (float32, default budget, stream mode)", "nranks": n,
+                      "rows": rows}), flush=True)
+
+
 def copy_probe(nbytes, reps):
     """A plain device-to-device copy of known size: reads and writes nbytes."""
     import torch
@@ -402,6 +463,8 @@ def main():
     ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-ceiling probes")
     ap.add_argument("--budget-sweep", action="store_true",
                     help="instead: time the workload at every aggregation level (T = 1 .. full)")
+    ap.add_argument("--size-sweep", action="store_true",
+                    help="instead: both collectives at N=128 over chunk sizes from 256 B (float32)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: all virtual ranks are emulated on one GPU; runs on more than one GPU "
@@ -415,6 +478,9 @@ def main():
         return
     if args.budget_sweep:
         budget_sweep(args.workload, args.steps)
+        return
+    if args.size_sweep:
+        size_sweep()
         return
 
     import synth
@@ -495,7 +561,8 @@ def main():
                    "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
                    "pat_steps": info["steps"], "pieces": info["pieces"],
                    "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"],
-                   "streaming_accesses": bool(info["streaming"]), "seed": seed},
+                   "streaming_accesses": bool(info["streaming"]), "xcd_order": bool(info["xcd_order"]),
+                   "seed": seed},
         "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),
         "latency_us": round(ms * 1e3, 2),
         "alg_bytes_per_op": info["alg_bytes"],

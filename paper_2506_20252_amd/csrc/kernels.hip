@@ -45,21 +45,15 @@
 
 #include "kernels.hpp"
 
-// Tuning knobs (compile time): vectors in flight per lane and the XCD-aware
-// work-item order.  Whether loads and stores stream (nontemporal) is a launch
-// argument, chosen per plan.
+// Tuning knobs (compile time): vectors in flight per lane.  Whether loads and
+// stores stream (nontemporal) and the work-item order are launch arguments,
+// chosen per plan.
 #ifndef PAT_UNROLL
 #define PAT_UNROLL 2
 #endif
 // bf16 reduce-scatter: 8-byte input vectors beside 16-byte float32 partials.
 #ifndef PAT_B16_UNROLL
 #define PAT_B16_UNROLL (2 * PAT_UNROLL)
-#endif
-// 1: workgroup b of a step takes work item (b % 8) * ceil(items / 8) + b / 8,
-// so that consecutive tiles (contiguous memory) run on one XCD (workgroups are
-// dispatched to the 8 XCDs round-robin).
-#ifndef PAT_XCD_SWIZZLE
-#define PAT_XCD_SWIZZLE 0
 #endif
 
 namespace pat {
@@ -589,16 +583,23 @@ struct RsOp {
 // ---------------------------------------------------------------------------
 
 // One launch per step; the step descriptor comes by value with the launch.
+// Work-item order: workgroups are dispatched to the 8 XCDs round-robin.  In
+// the plain order, consecutive workgroups (consecutive tiles of an edge) land
+// on different XCDs and all XCDs sweep the same few edges together; in the
+// XCD order (xcd != 0, grid = 8 * ceil(items / 8)) workgroup b takes item
+// (b % 8) * ceil(items / 8) + b / 8, so each XCD works through its own
+// contiguous eighth of the step.
+// One call site for Op::run: a second inlined copy of the bf16 op pushed the
+// compiler into scratch memory.
 template <class Op>
-__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st) {
-  if (PAT_XCD_SWIZZLE) {
-    // grid = 8 * ceil(items / 8) (no grid-stride): see launch_step_t
+__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int xcd) {
+  int64_t item = blockIdx.x, stride = gridDim.x;
+  if (xcd) {
     const int64_t q = (st.items + 7) / 8;
-    const int64_t item = (int64_t)(blockIdx.x % 8) * q + blockIdx.x / 8;
-    if (item < st.items) Op::run(cx, st, item);
-    return;
+    item = (int64_t)(blockIdx.x % 8) * q + blockIdx.x / 8;
+    stride = st.items;  // at most one item per workgroup
   }
-  for (int64_t item = blockIdx.x; item < st.items; item += gridDim.x) Op::run(cx, st, item);
+  for (; item < st.items; item += stride) Op::run(cx, st, item);
 }
 
 // Fused top part of the schedule: one workgroup per (tree, tile of its
@@ -798,16 +799,17 @@ __global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
 }
 
 template <class Op>
-hipError_t launch_step_t(const KCtx& cx, const DevStep& st, hipStream_t stream) {
+hipError_t launch_step_t(const KCtx& cx, const DevStep& st, bool xcd_order, hipStream_t stream) {
   const int64_t items = st.items;
   if (items <= 0) return hipSuccess;
   const int64_t cap = int64_t(1) << 30;
   unsigned grid = (unsigned)(items < cap ? items : cap);
-  if (PAT_XCD_SWIZZLE) {
-    if (items > cap) return hipErrorInvalidValue;
-    grid = (unsigned)((items + 7) / 8 * 8);
+  if (xcd_order && items <= cap) {
+    grid = (unsigned)((items + 7) / 8 * 8);  // every workgroup gets at most one item
+  } else {
+    xcd_order = false;  // beyond one grid the plain order strides over the items
   }
-  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, st);
+  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, st, xcd_order ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -878,8 +880,9 @@ int variant_tile(Variant v) {
 
 #define PAT_UNPAREN(...) __VA_ARGS__
 
-hipError_t launch_step(Variant v, bool streaming, const KCtx& cx, const DevStep& st, hipStream_t stream) {
-#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, stream)
+hipError_t launch_step(Variant v, bool streaming, bool xcd_order, const KCtx& cx, const DevStep& st,
+                       hipStream_t stream) {
+#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, xcd_order, stream)
   PAT_DISPATCH(v, streaming, PAT_STEP)
 #undef PAT_STEP
 }

@@ -61,7 +61,10 @@ int variant_tile(Variant v);
 // streaming: nontemporal loads and stores, for operations much larger than
 // the 256 MB Infinity Cache; plain accesses let a small operation's steps
 // hit in it (each step reads the slots the previous one wrote).
-hipError_t launch_step(Variant v, bool streaming, const KCtx& cx, const DevStep& st, hipStream_t stream);
+// xcd_order: each XCD takes a contiguous eighth of the step's work items
+// instead of every eighth one (see step_kernel).
+hipError_t launch_step(Variant v, bool streaming, bool xcd_order, const KCtx& cx, const DevStep& st,
+                       hipStream_t stream);
 // Fused top part: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
 struct TreeRange {
