@@ -561,7 +561,7 @@ def main():
                    "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
                    "pat_steps": info["steps"], "pieces": info["pieces"],
                    "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"],
-                   "streaming_accesses": bool(info["streaming"]), "xcd_order": bool(info["xcd_order"]),
+                   "streaming_accesses": bool(info["streaming"]), "xcd_run": info["xcd_run"],
                    "seed": seed},
         "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),
         "latency_us": round(ms * 1e3, 2),

@@ -194,7 +194,8 @@ typedef struct {
   int fused_top_steps;        /* steps run as one fused launch (stream/graph modes, current setting) */
   int launches_per_op;        /* kernel launches per operation in stream mode (128-bit path if possible) */
   int streaming;              /* 1: nontemporal loads and stores (operations of >= 1e9 algorithmic bytes) */
-  int xcd_order;              /* 1: each XCD takes a contiguous eighth of a step's work (all-gather) */
+  int xcd_run;                /* step kernels: each XCD takes runs of this many consecutive work items
+                                 (0: a contiguous eighth of each step; all-gather 0, reduce-scatter 32) */
 } pat_plan_info_t;
 
 pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,

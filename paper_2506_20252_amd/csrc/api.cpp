@@ -137,15 +137,18 @@ int blocks_per_cu_cap(double bytes_per_step) {
 // streaming ones 8-12% faster far above).  PAT_STREAMING=0/1 overrides.
 constexpr double kStreamingBytes = 1e9;
 
-// Work-item order of the step kernels.  Measured on MI355X: all-gather steps
-// (up to two bytes written per byte read) run up to 24% faster when each XCD
-// works through its own contiguous eighth of the step; reduce-scatters run
-// 1-5% faster with all XCDs sweeping the same edges together.
-// PAT_XCD_ORDER=0/1 overrides.
-bool xcd_order_for(int coll) {
-  if (const char* e = std::getenv("PAT_XCD_ORDER")) return e[0] == '1';
-  return coll == 0;
+// Work-item order of the step kernels: each XCD takes runs of this many
+// consecutive work items (0: a contiguous eighth of the step).  Measured on
+// MI355X against the plain order (runs of 1): all-gather steps, which write
+// up to two bytes per byte read, run up to 24% faster with a contiguous
+// eighth per XCD; reduce-scatter steps 1-7% faster with runs of 32 (16-32
+// are alike).  PAT_XCD_GRAIN overrides (a count of items; tuning).
+int64_t xcd_run_for(int coll) {
+  if (const char* e = std::getenv("PAT_XCD_GRAIN")) return std::max(0LL, std::atoll(e));
+  return coll == 0 ? 0 : 32;
 }
+
+int64_t xcd_grain(int64_t run) { return run > 0 ? run : (int64_t(1) << 40); }
 
 bool streaming_for(double alg_bytes) {
   if (const char* e = std::getenv("PAT_STREAMING")) return e[0] == '1';
@@ -189,7 +192,7 @@ struct Plan {
   std::map<std::tuple<int, int, int, int>, hipGraphExec_t> graphs;
   int capacity[pat::kNumVariants][2] = {};
   bool streaming = true;
-  bool xcd_order = false;  // step kernels: each XCD takes a contiguous eighth of a step
+  int64_t xcd_run = 1;     // step kernels: work items per XCD run (0: a contiguous eighth)
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
   int cus = 0;
   int64_t clock_khz = 0;
@@ -301,7 +304,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
   p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
   p->streaming = streaming_for(d.alg_bytes);
-  p->xcd_order = xcd_order_for(coll);
+  p->xcd_run = xcd_run_for(coll);
   p->alg_bytes = d.alg_bytes;
 
   p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
@@ -526,7 +529,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
           s = tr.s1 - 1;
           continue;
         }
-        const hipError_t e = pat::launch_step(var, plan->streaming, plan->xcd_order, cx, steps[s], q);
+        const hipError_t e = pat::launch_step(var, plan->streaming, xcd_grain(plan->xcd_run), cx, steps[s], q);
         if (e != hipSuccess) return e;
       }
       return hipSuccess;
@@ -682,7 +685,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
     info.launches_per_op = int(d.exec.size()) * d.pieces - (s1 > s0 ? s1 - s0 - 1 : 0);
   }
   info.streaming = streaming_for(d.alg_bytes) ? 1 : 0;
-  info.xcd_order = xcd_order_for((int)coll) ? 1 : 0;
+  info.xcd_run = (int)std::min<int64_t>(xcd_run_for((int)coll), INT32_MAX);
   *out = info;
   return PAT_OK;
 }

@@ -583,22 +583,22 @@ struct RsOp {
 // ---------------------------------------------------------------------------
 
 // One launch per step; the step descriptor comes by value with the launch.
-// Work-item order: workgroups are dispatched to the 8 XCDs round-robin.  In
-// the plain order, consecutive workgroups (consecutive tiles of an edge) land
-// on different XCDs and all XCDs sweep the same few edges together; in the
-// XCD order (xcd != 0, grid = 8 * ceil(items / 8)) workgroup b takes item
-// (b % 8) * ceil(items / 8) + b / 8, so each XCD works through its own
-// contiguous eighth of the step.
-// One call site for Op::run: a second inlined copy of the bf16 op pushed the
-// compiler into scratch memory.
+// Work-item order: workgroups are dispatched to the 8 XCDs round-robin, and
+// with grain g each XCD takes runs of g consecutive work items (consecutive
+// tiles of an edge): workgroup b, on XCD x = b % 8 as its j-th = b / 8,
+// takes item (j / g) * 8g + x * g + j % g.  g = 1 is the plain order (all
+// XCDs sweep the same few edges together); g = ceil(items / 8) gives each XCD
+// a contiguous eighth of the step.  The grid is a multiple of 8g.
 template <class Op>
-__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int xcd) {
+__global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int64_t grain) {
   int64_t item = blockIdx.x, stride = gridDim.x;
-  if (xcd) {
-    const int64_t q = (st.items + 7) / 8;
-    item = (int64_t)(blockIdx.x % 8) * q + blockIdx.x / 8;
+  if (grain > 1) {
+    const int64_t x = blockIdx.x % 8, j = blockIdx.x / 8;
+    item = (j / grain) * 8 * grain + x * grain + j % grain;
     stride = st.items;  // at most one item per workgroup
   }
+  // One call site for Op::run: a second inlined copy of the bf16 op pushed
+  // the compiler into scratch memory.
   for (; item < st.items; item += stride) Op::run(cx, st, item);
 }
 
@@ -799,17 +799,21 @@ __global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
 }
 
 template <class Op>
-hipError_t launch_step_t(const KCtx& cx, const DevStep& st, bool xcd_order, hipStream_t stream) {
+hipError_t launch_step_t(const KCtx& cx, const DevStep& st, int64_t grain, hipStream_t stream) {
   const int64_t items = st.items;
   if (items <= 0) return hipSuccess;
   const int64_t cap = int64_t(1) << 30;
   unsigned grid = (unsigned)(items < cap ? items : cap);
-  if (xcd_order && items <= cap) {
-    grid = (unsigned)((items + 7) / 8 * 8);  // every workgroup gets at most one item
-  } else {
-    xcd_order = false;  // beyond one grid the plain order strides over the items
+  if (grain > 1) {
+    grain = grain < (items + 7) / 8 ? grain : (items + 7) / 8;  // beyond a contiguous eighth is the same
+    const int64_t run = 8 * grain;
+    const int64_t g = (items + run - 1) / run * run;
+    if (g <= cap)
+      grid = (unsigned)g;  // every workgroup gets at most one item
+    else
+      grain = 1;  // beyond one grid the plain order strides over the items
   }
-  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, st, xcd_order ? 1 : 0);
+  hipLaunchKernelGGL(step_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, st, grain);
   return hipGetLastError();
 }
 
@@ -880,9 +884,9 @@ int variant_tile(Variant v) {
 
 #define PAT_UNPAREN(...) __VA_ARGS__
 
-hipError_t launch_step(Variant v, bool streaming, bool xcd_order, const KCtx& cx, const DevStep& st,
+hipError_t launch_step(Variant v, bool streaming, int64_t grain, const KCtx& cx, const DevStep& st,
                        hipStream_t stream) {
-#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, xcd_order, stream)
+#define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, grain, stream)
   PAT_DISPATCH(v, streaming, PAT_STEP)
 #undef PAT_STEP
 }

@@ -61,9 +61,9 @@ int variant_tile(Variant v);
 // streaming: nontemporal loads and stores, for operations much larger than
 // the 256 MB Infinity Cache; plain accesses let a small operation's steps
 // hit in it (each step reads the slots the previous one wrote).
-// xcd_order: each XCD takes a contiguous eighth of the step's work items
-// instead of every eighth one (see step_kernel).
-hipError_t launch_step(Variant v, bool streaming, bool xcd_order, const KCtx& cx, const DevStep& st,
+// grain: each XCD takes runs of this many consecutive work items (1: every
+// eighth item; large: a contiguous eighth of the step; see step_kernel).
+hipError_t launch_step(Variant v, bool streaming, int64_t grain, const KCtx& cx, const DevStep& st,
                        hipStream_t stream);
 // Fused top part: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).

@@ -285,12 +285,12 @@ def test_streaming_choice_reported_by_plan_info(monkeypatch):
         assert st == pat.PAT_OK
         assert info["streaming"] == want, args
         assert (info["alg_bytes"] >= 1e9) == bool(want)
-    # work order: XCD-contiguous for all-gathers
-    for args, want in (((pat.PAT_REDUCESCATTER, 128, 2 << 20, "bfloat16"), 0),
-                       ((pat.PAT_REDUCESCATTER, 1000, 64, "float32"), 0),
-                       ((pat.PAT_ALLGATHER, 64, 262144, "float32"), 1),
-                       ((pat.PAT_ALLGATHER, 24, 32768, "bfloat16"), 1)):
-        assert pat.pat_plan_info(*args)[1]["xcd_order"] == want, args
+    # work order: a contiguous eighth per XCD for all-gathers (0), runs of 32 for reduce-scatters
+    for args, want in (((pat.PAT_REDUCESCATTER, 128, 2 << 20, "bfloat16"), 32),
+                       ((pat.PAT_REDUCESCATTER, 1000, 64, "float32"), 32),
+                       ((pat.PAT_ALLGATHER, 64, 262144, "float32"), 0),
+                       ((pat.PAT_ALLGATHER, 24, 32768, "bfloat16"), 0)):
+        assert pat.pat_plan_info(*args)[1]["xcd_run"] == want, args
     monkeypatch.setenv("PAT_STREAMING", "1")
     assert pat.pat_plan_info(pat.PAT_ALLGATHER, 24, 32768, "bfloat16")[1]["streaming"] == 1
     monkeypatch.setenv("PAT_STREAMING", "0")
