@@ -553,3 +553,24 @@ def test_top_fusion_with_odd_tiles(tile, monkeypatch):
                          oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
     finally:
         pat.check(pat.pat_set_top_fusion("auto"))
+
+
+@pytest.mark.parametrize("grain", ["1", "3", "7", "1000"])
+def test_xcd_run_lengths(grain, monkeypatch):
+    """The step kernels' XCD work order with run lengths that divide nothing:
+    every work item is still done exactly once (the grid is padded to a
+    multiple of 8 runs and the surplus workgroups have no item)."""
+    monkeypatch.setenv("PAT_XCD_GRAIN", grain)
+    pat.check(pat.pat_finalize())  # the run length is fixed when a plan is made
+    try:
+        for n, count in ((13, 1000), (7, 20004), (33, 17)):
+            for dtype in ("int32", "float32", "bfloat16"):
+                seed = 53 * n + count + int(grain)
+                got, host_in = run_ag(n, count, dtype, seed, mode="stream")
+                np.testing.assert_array_equal(got, D.allgather(host_in))
+                got = run_rs(n, count, dtype, seed + 1, mode="stream")
+                check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+                         oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+    finally:
+        monkeypatch.delenv("PAT_XCD_GRAIN")
+        pat.check(pat.pat_finalize())
