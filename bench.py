@@ -198,7 +198,7 @@ def small_size_latency(reps=200):
         st, info = pat.pat_plan_info(code, n, count, "float32")
         out[f"{coll}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
         out["steps"] = info["steps"]
-        out[f"{coll}_launches"] = info["launches_per_op"]  # the top part's far steps run as one launch
+        out[f"{coll}_launches"] = info["launches_per_op"]  # the far fusable steps run as one launch
         del send, recv, S, R
     torch.cuda.empty_cache()
     return out
@@ -560,7 +560,7 @@ def main():
                    "collective": "reduce-scatter" if coll == "rs" else "all-gather", "exec_mode": args.mode,
                    "buffer_bytes_per_slot": pat.pat_get_buffer_bytes(), "T": info["T"],
                    "pat_steps": info["steps"], "pieces": info["pieces"],
-                   "fused_top_steps": 0 if args.mode == "persistent" else info["fused_top_steps"],
+                   "fused_steps": 0 if args.mode == "persistent" else info["fused_steps"],
                    "streaming_accesses": bool(info["streaming"]), "xcd_run": info["xcd_run"],
                    "seed": seed},
         "bus_gbps_per_rank": round(bus_per_rank / sec / 1e9, 4),

@@ -65,7 +65,7 @@ int fusion_now() {
   return PAT_FUSION_AUTO;
 }
 
-// Vectors of a chunk per workgroup of the fused top part (each tree's chain
+// Vectors of a chunk per workgroup of a fused range (each tree's chain
 // is sequential inside its workgroup; smaller tiles give more workgroups but
 // measured slower on 64 KiB chunks).  Tuning overrides come from the
 // environment (positive integers only).
@@ -78,7 +78,7 @@ int64_t env_or(const char* name, int64_t dflt) {
 }
 int64_t tree_tile_vecs() { return env_or("PAT_TREE_TILE", 256); }
 
-// PAT_FUSION_AUTO fuses the far end of the top part: the steps that move at
+// PAT_FUSION_AUTO fuses the far end of the fusable steps: those that move at
 // most this many bytes (short, latency-bound steps) and whose edges of one
 // tree, times the vectors of one tile, fit a few load rounds per lane.
 // Larger steps keep a kernel each, which spreads their edges over the whole
@@ -87,16 +87,21 @@ int64_t tree_fuse_vecs() { return env_or("PAT_TREE_FUSE_VECS", 2048); }
 int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(64) << 20); }
 
 // Launch-level steps [*s0, *s1) that run as one fused launch, for a plan whose
-// chunk-pieces hold V vectors; empty when nothing is fused.  The top part is
-// the first t steps of the all-gather order and the last t of the
-// reduce-scatter's; AUTO keeps its narrow far end (the reduce-scatter's last
-// steps, the all-gather's first: chunks per rank grow toward the middle).
+// chunk-pieces hold V vectors; empty when nothing is fused.  The candidates
+// are the steps whose slot entries each serve one tree: the top part (the
+// first t steps of the all-gather order, the last t of the reduce-scatter's),
+// and at full aggregation (sub-trees of span M = 2) the whole schedule, since
+// its one linear step, at distance 1, ends at leaves (all-gather) or starts
+// from them (reduce-scatter).  AUTO keeps the narrow far end (the
+// reduce-scatter's last steps, the all-gather's first: chunks per rank grow
+// toward the near end).
 void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1, int64_t* tile_vecs) {
   *s0 = *s1 = 0;
   *tile_vecs = std::max<int64_t>(1, std::min<int64_t>(V, tree_tile_vecs()));
-  if (fusion == PAT_FUSION_OFF || d.pieces != 1 || d.sched.t < 2) return;
+  if (fusion == PAT_FUSION_OFF || d.pieces != 1) return;
   const int ns = (int)d.exec.size(), t = d.sched.t;
-  int lo = d.coll == 0 ? 0 : ns - t, hi = d.coll == 0 ? t : ns;
+  const bool whole = d.sched.M <= 2;
+  int lo = whole || d.coll == 0 ? 0 : ns - t, hi = whole || d.coll == 1 ? ns : t;
   if (fusion == PAT_FUSION_AUTO) {
     const int64_t cap = tree_fuse_vecs(), cap_bytes = tree_fuse_bytes();
     // bytes a step moves: about three chunk transfers per edge
@@ -515,8 +520,8 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
                      capacity, plan->cus, grid, cx.nsteps);
     HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
   } else {
-    // Stream and graph modes: one kernel per step, except that the top part
-    // may run as one fused launch.
+    // Stream and graph modes: one kernel per step, except that a range of
+    // steps whose slot entries each serve one tree may run as one launch.
     pat::TreeRange tr{};
     fused_range(d, steps.empty() ? 0 : steps[0].V, fusion_now(), &tr.s0, &tr.s1, &tr.tile_vecs);
     const bool fuse = tr.s1 > tr.s0;
@@ -681,7 +686,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
     int64_t tile;
     std::lock_guard<std::mutex> lock(g_mu);
     fused_range(d, V, fusion_now(), &s0, &s1, &tile);
-    info.fused_top_steps = s1 - s0;
+    info.fused_steps = s1 - s0;
     info.launches_per_op = int(d.exec.size()) * d.pieces - (s1 > s0 ? s1 - s0 - 1 : 0);
   }
   info.streaming = streaming_for(d.alg_bytes) ? 1 : 0;

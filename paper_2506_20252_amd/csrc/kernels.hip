@@ -36,8 +36,9 @@
 // at step s + 1).  Per-step launches get the ordering from the kernel
 // boundary; the persistent kernel orders its work queue by per-step
 // completion counters whose fences make every workgroup's writes visible
-// across the XCDs' separate L2 caches; the fused top part (tree_kernel) needs
-// only workgroup barriers, since there each tree's data is its workgroup's.
+// across the XCDs' separate L2 caches; a fused range of steps (tree_kernel)
+// needs only workgroup barriers, since there each tree's data is its
+// workgroup's.
 
 #include <hip/hip_runtime.h>
 
@@ -127,7 +128,7 @@ __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int*
   *i = (int)(e - (int64_t)(*r) * st.k);
 }
 
-// Workgroup size of the fused top part.  A tree's steps run one after another
+// Workgroup size of a fused range of steps.  A tree's steps run one after another
 // inside its workgroup, so a wide workgroup covers a whole step in fewer load
 // rounds (a shorter chain of dependent accesses per step).
 #ifndef PAT_TREE_THREADS
@@ -136,7 +137,7 @@ __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int*
 constexpr int kTreeThreads = PAT_TREE_THREADS;
 static_assert(kTreeThreads % 64 == 0 && kTreeThreads <= 1024, "tree workgroup: whole wavefronts, at most 1024 lanes");
 
-// One step of one tree in a fused top part: the pairs (entry i, vector v)
+// One step of one tree in a fused range: the pairs (entry i, vector v)
 // with i < k and v in [t0, t0 + TV), flattened vector-fastest so that lanes
 // sweep each edge's tile contiguously, U pairs per lane at a time.
 template <class Op>
@@ -602,10 +603,11 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int
   for (; item < st.items; item += stride) Op::run(cx, st, item);
 }
 
-// Fused top part of the schedule: one workgroup per (tree, tile of its
-// chunk) runs the launch-level steps s0 .. s1 - 1 in order.  In the top part
-// every slot entry is used once and by one tree only, so the data a step of
-// tree c reads was written by an earlier step of tree c: by this workgroup.
+// Fused range of steps: one workgroup per (tree, tile of its chunk) runs the
+// launch-level steps s0 .. s1 - 1 in order.  The range holds only steps whose
+// slot entries each serve one tree (the top part; at full aggregation every
+// step), so the data a step of tree c reads was written by an earlier step of
+// tree c, over the same tile: by this workgroup.
 // A workgroup barrier between steps then replaces the kernel boundary; each
 // wave first waits for its own stores.
 template <class Op>

@@ -65,7 +65,7 @@ int variant_tile(Variant v);
 // eighth item; large: a contiguous eighth of the step; see step_kernel).
 hipError_t launch_step(Variant v, bool streaming, int64_t grain, const KCtx& cx, const DevStep& st,
                        hipStream_t stream);
-// Fused top part: launch-level steps [s0, s1) of one piece, run by one
+// Fused range: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
 struct TreeRange {
   int32_t s0, s1;

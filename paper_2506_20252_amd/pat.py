@@ -68,7 +68,7 @@ class pat_plan_info_t(ctypes.Structure):
         ("slot_elem_bytes", ctypes.c_size_t), ("slot_dims", ctypes.c_int),
         ("slot_chunks_per_rank", ctypes.c_int), ("slot_bytes_per_rank", ctypes.c_size_t),
         ("slot_bytes_total", ctypes.c_size_t), ("alg_bytes", ctypes.c_double),
-        ("bus_bytes_per_rank", ctypes.c_double), ("fused_top_steps", ctypes.c_int),
+        ("bus_bytes_per_rank", ctypes.c_double), ("fused_steps", ctypes.c_int),
         ("launches_per_op", ctypes.c_int), ("streaming", ctypes.c_int), ("xcd_run", ctypes.c_int),
     ]
 

@@ -372,7 +372,8 @@ def test_plan_cache_is_bounded_and_evicts_safely():
 
 
 # ---------------------------------------------------------------------------
-# Fused top part: one workgroup per (tree, tile) runs the top t steps
+# Fused steps: one workgroup per (tree, tile) runs the top t steps (at full
+# aggregation, every step)
 # ---------------------------------------------------------------------------
 
 
@@ -415,6 +416,36 @@ def test_top_fusion_is_bit_identical_to_step_kernels(n, count, dtype):
     for fusion in ("on", "auto"):
         np.testing.assert_array_equal(outs[fusion][0], outs["off"][0])
         np.testing.assert_array_equal(outs[fusion][1], outs["off"][1])
+
+
+@pytest.mark.parametrize("n", [3, 5, 8, 9, 24, 31, 65, 129, 1000])
+@pytest.mark.parametrize("count", [5, 300, 4100])
+def test_whole_schedule_fused_at_full_aggregation(n, count):
+    """At full aggregation (sub-trees of span 2) every step joins the fused
+    launch, the distance-1 step included: one launch per operation, same
+    results as the oracle and the same bits as one kernel per step."""
+    seed = 0xF0 + 7 * n + count
+    try:
+        for dtype in ("int32", "float32", "bfloat16"):
+            if n == 1000 and dtype != "float32":
+                continue  # keep the case small; the float32 run covers the shape
+            outs = {}
+            for fusion in ("on", "off"):
+                pat.check(pat.pat_set_top_fusion(fusion))
+                for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+                    st, info = pat.pat_plan_info(coll, n, count, dtype)
+                    assert st == pat.PAT_OK and info["t"] == info["L"] - 1
+                    assert info["fused_steps"] == (info["steps"] if fusion == "on" else 0)
+                mode = "graph" if n == 24 else "stream"
+                outs[fusion] = (run_ag(n, count, dtype, seed, mode=mode), run_rs(n, count, dtype, seed + 1, mode=mode))
+            got, host_in = outs["on"][0]
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+            check_rs(outs["on"][1], host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+            np.testing.assert_array_equal(outs["on"][0][0], outs["off"][0][0])
+            np.testing.assert_array_equal(outs["on"][1], outs["off"][1])
+    finally:
+        pat.check(pat.pat_set_top_fusion("auto"))
 
 
 def test_workload3_and_2_with_fusion_forced_on():

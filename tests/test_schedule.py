@@ -251,24 +251,31 @@ def test_top_fusion_setting_roundtrip():
 
 @pytest.mark.parametrize("coll", [pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER])
 def test_fused_range_reported_by_plan_info(coll):
-    """Which steps run as one fused launch (stream and graph modes): N=1000
-    with 256-byte chunks fuses the 7 narrow far steps of the top part (16
-    vectors x at most 62 chunks <= 1024), N=6 with 4 KiB chunks its 2 top
-    steps; a top part of one step is never fused."""
+    """Which steps run as one fused launch (stream and graph modes).  Both
+    plans are fully aggregated, so every step may fuse: N=1000 with 256-byte
+    chunks fuses (AUTO) the 7 narrow far steps (at most 62 chunks per rank;
+    the next moves 3 x 1000 x 125 x 256 B > 64 MiB) or (ON) all 10; N=6 with 4 KiB chunks all 3 steps (256
+    vectors x at most 3 chunks).  A plan with a wider linear part fuses its
+    top part only, and a top part of one step is never fused."""
     try:
-        for fusion, want in (("auto", (7, 4)), ("on", (9, 2)), ("off", (0, 10))):
+        for fusion, want in (("auto", (7, 4)), ("on", (10, 1)), ("off", (0, 10))):
             pat.check(pat.pat_set_top_fusion(fusion))
             st, info = pat.pat_plan_info(coll, 1000, 64, "float32")
             assert st == pat.PAT_OK and info["steps"] == 10 and info["t"] == 9
-            assert (info["fused_top_steps"], info["launches_per_op"]) == want
+            assert (info["fused_steps"], info["launches_per_op"]) == want
         pat.check(pat.pat_set_top_fusion("auto"))
         st, info = pat.pat_plan_info(coll, 6, 1024, "int32")
-        assert (info["t"], info["fused_top_steps"], info["launches_per_op"]) == (2, 2, 2)
+        assert (info["t"], info["fused_steps"], info["launches_per_op"]) == (2, 3, 1)
+        # N=64, 1 MiB float32 chunks: T = 8 sub-trees of span 8; ON fuses the 3 top steps
+        pat.check(pat.pat_set_top_fusion("on"))
+        st, info = pat.pat_plan_info(coll, 64, 1 << 18, "float32")
+        assert (info["t"], info["steps"], info["fused_steps"], info["launches_per_op"]) == (3, 10, 3, 8)
+        pat.check(pat.pat_set_top_fusion("auto"))
         # 4 MiB bf16 chunks: the all-gather's slots hold bf16 (T = 2, 64 steps, one top step),
         # the reduce-scatter's hold float32 partials (T = 1, 127 steps, no top part)
         st, info = pat.pat_plan_info(coll, 128, 2 << 20, "bfloat16")
         want = (1, 0, 64) if coll == pat.PAT_ALLGATHER else (0, 0, 127)
-        assert (info["t"], info["fused_top_steps"], info["launches_per_op"]) == want
+        assert (info["t"], info["fused_steps"], info["launches_per_op"]) == want
     finally:
         pat.check(pat.pat_set_top_fusion("auto"))
 
@@ -313,3 +320,26 @@ def test_large_rank_counts_match_oracle(n):
                 assert len(steps) == (L if t == L - 1 else n - 1)
     finally:
         pat.pat_set_buffer_bytes(0)
+
+
+@pytest.mark.parametrize("order", ["far", "close"])
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 7, 8, 9, 16, 24, 33, 64, 100, 129, 1000])
+def test_full_aggregation_every_slot_serves_one_tree(n, order):
+    """At full aggregation (T = 2^(L-1), sub-trees of span 2) the linear part
+    is one distance-1 step whose receivers are leaves (all-gather) or top
+    positions (reduce-scatter), so every slot entry of the whole schedule
+    serves one tree: all steps may run as one fused launch."""
+    count = 64
+    pat.check(pat.pat_set_linear_order(order))
+    try:
+        L = opat.ceil_log2(n)
+        pat.pat_set_buffer_bytes(budget_for(n, max(L - 1, 0), count * 4))
+        for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+            st, info = pat.pat_plan_info(coll, n, count, "float32")
+            assert info["t"] == max(L - 1, 0)
+            _, steps, entries = library_steps(coll, n, count, "float32")
+            use = _slot_trees(coll, n, steps, entries, 0, len(steps))
+            assert all(len(trees) == 1 for trees in use.values()), coll
+    finally:
+        pat.pat_set_buffer_bytes(0)
+        pat.pat_set_linear_order("far")
