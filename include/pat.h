@@ -152,18 +152,19 @@ int pat_get_exec_mode(void);
  * steps (the fully aggregated distances, section "The PAT algorithm") every
  * intermediate-buffer entry serves a single tree, so one workgroup per (tree,
  * tile of its chunk) can run all of them with workgroup barriers instead of
- * one kernel per step.  At full aggregation (T = 2^(L-1), sub-trees of span
- * 2) the same holds for the whole schedule: its one linear step, at distance
- * 1, ends at leaves (all-gather) or starts from them (reduce-scatter), and
- * joins the fusable range.  The edges, bytes and summation order are
- * unchanged.  A workgroup runs its tree's steps one after another, so wide
- * steps (many chunks per rank) are better left to one kernel each.  AUTO (the
- * default, or the PAT_TOP_FUSION environment variable: auto | on | off) fuses
- * the far end of the fusable range, the steps that move at most 64 MiB and in
- * which one tree's edges over one tile of its chunk (256 vectors) amount to
- * at most 2048 vectors, when there are two or more such steps; ON fuses the
- * whole fusable range whenever it has two or more steps.  Neither fuses a
- * chunk that is split into pieces.
+ * one kernel per step.  When the sub-trees span at most 4 (T >= 2^(L-2)) the
+ * same holds for the whole schedule, whose linear steps then join the
+ * fusable range: a linear-part node keeps its chunk at index p / 4 of its
+ * distance's slot, used by position p alone, and leaves keep nothing.  The
+ * edges, bytes and summation order are unchanged.  A workgroup runs its
+ * tree's steps one after another, so wide steps (many chunks per rank) are
+ * better left to one kernel each.  AUTO (the default, or the PAT_TOP_FUSION
+ * environment variable: auto | on | off) fuses the far end of the fusable
+ * range, the steps that move at most 64 MiB and in which one tree's edges
+ * over one tile of its chunk (256 vectors) amount to at most 2048 vectors,
+ * when there are two or more such steps; ON fuses the whole fusable range
+ * whenever it has two or more steps.  Neither fuses a chunk that is split
+ * into pieces.
  */
 typedef enum { PAT_FUSION_AUTO = 0, PAT_FUSION_OFF = 1, PAT_FUSION_ON = 2 } pat_fusion_t;
 pat_status_t pat_set_top_fusion(int mode);

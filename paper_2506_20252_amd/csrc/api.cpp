@@ -90,17 +90,18 @@ int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(64) << 
 // chunk-pieces hold V vectors; empty when nothing is fused.  The candidates
 // are the steps whose slot entries each serve one tree: the top part (the
 // first t steps of the all-gather order, the last t of the reduce-scatter's),
-// and at full aggregation (sub-trees of span M = 2) the whole schedule, since
-// its one linear step, at distance 1, ends at leaves (all-gather) or starts
-// from them (reduce-scatter).  AUTO keeps the narrow far end (the
-// reduce-scatter's last steps, the all-gather's first: chunks per rank grow
-// toward the near end).
+// and the whole schedule when the sub-trees span M <= 4.  There a linear-part
+// node at position p keeps its chunk at index p / 4 of its distance's slot,
+// which only p = 4 idx + 2 uses (distance 2), and leaves keep nothing; from
+// M = 8 on, positions 8 idx + 2 and 8 idx + 6 share a distance-2 entry.  AUTO
+// keeps the narrow far end (the reduce-scatter's last steps, the
+// all-gather's first: chunks per rank grow toward the near end).
 void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1, int64_t* tile_vecs) {
   *s0 = *s1 = 0;
   *tile_vecs = std::max<int64_t>(1, std::min<int64_t>(V, tree_tile_vecs()));
   if (fusion == PAT_FUSION_OFF || d.pieces != 1) return;
   const int ns = (int)d.exec.size(), t = d.sched.t;
-  const bool whole = d.sched.M <= 2;
+  const bool whole = d.sched.M <= 4;
   int lo = whole || d.coll == 0 ? 0 : ns - t, hi = whole || d.coll == 1 ? ns : t;
   if (fusion == PAT_FUSION_AUTO) {
     const int64_t cap = tree_fuse_vecs(), cap_bytes = tree_fuse_bytes();

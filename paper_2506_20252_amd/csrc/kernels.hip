@@ -605,8 +605,8 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int
 
 // Fused range of steps: one workgroup per (tree, tile of its chunk) runs the
 // launch-level steps s0 .. s1 - 1 in order.  The range holds only steps whose
-// slot entries each serve one tree (the top part; at full aggregation every
-// step), so the data a step of tree c reads was written by an earlier step of
+// slot entries each serve one tree (the top part; every step when the
+// sub-trees span at most 4), so the data a step of tree c reads was written by an earlier step of
 // tree c, over the same tile: by this workgroup.
 // A workgroup barrier between steps then replaces the kernel boundary; each
 // wave first waits for its own stores.

@@ -418,34 +418,59 @@ def test_top_fusion_is_bit_identical_to_step_kernels(n, count, dtype):
         np.testing.assert_array_equal(outs[fusion][1], outs["off"][1])
 
 
+def _max_chunks(n, t):
+    return max(len(P) for _, P in opat.schedule(n, t))
+
+
+@pytest.mark.parametrize("span", [2, 4])
 @pytest.mark.parametrize("n", [3, 5, 8, 9, 24, 31, 65, 129, 1000])
 @pytest.mark.parametrize("count", [5, 300, 4100])
-def test_whole_schedule_fused_at_full_aggregation(n, count):
-    """At full aggregation (sub-trees of span 2) every step joins the fused
-    launch, the distance-1 step included: one launch per operation, same
-    results as the oracle and the same bits as one kernel per step."""
-    seed = 0xF0 + 7 * n + count
+def test_whole_schedule_fused_up_to_span_4(n, count, span):
+    """With sub-trees of span 2 (full aggregation) or 4 every step joins the
+    fused launch, the linear part included: one launch per operation, the
+    oracle's results, and the same bits as one kernel per step."""
+    L = opat.ceil_log2(n)
+    t = L - (1 if span == 2 else 2)
+    if t < 0 or (n, span) == (3, 4) or (n == 1000 and count == 4100):
+        # N = 3 reaches full aggregation on the budget of span 4
+        pytest.skip("no such level / keep the case small")
+    seed = 0xF0 + 7 * n + count + span
+    ran = 0
     try:
         for dtype in ("int32", "float32", "bfloat16"):
             if n == 1000 and dtype != "float32":
                 continue  # keep the case small; the float32 run covers the shape
-            outs = {}
-            for fusion in ("on", "off"):
-                pat.check(pat.pat_set_top_fusion(fusion))
-                for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
-                    st, info = pat.pat_plan_info(coll, n, count, dtype)
-                    assert st == pat.PAT_OK and info["t"] == info["L"] - 1
+            for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+                slot = 4 if (coll == pat.PAT_REDUCESCATTER or dtype != "bfloat16") else 2
+                pat.check(pat.pat_set_buffer_bytes(_max_chunks(n, t) * count * slot))
+                st, info = pat.pat_plan_info(coll, n, count, dtype)
+                assert st == pat.PAT_OK
+                if info["t"] != t or info["steps"] < 2:
+                    continue  # truncation let this budget reach the next level
+                outs = {}
+                for fusion in ("on", "off"):
+                    pat.check(pat.pat_set_top_fusion(fusion))
+                    _, info = pat.pat_plan_info(coll, n, count, dtype)
                     assert info["fused_steps"] == (info["steps"] if fusion == "on" else 0)
-                mode = "graph" if n == 24 else "stream"
-                outs[fusion] = (run_ag(n, count, dtype, seed, mode=mode), run_rs(n, count, dtype, seed + 1, mode=mode))
-            got, host_in = outs["on"][0]
-            np.testing.assert_array_equal(got, D.allgather(host_in))
-            check_rs(outs["on"][1], host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
-                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
-            np.testing.assert_array_equal(outs["on"][0][0], outs["off"][0][0])
-            np.testing.assert_array_equal(outs["on"][1], outs["off"][1])
+                    mode = "graph" if n == 24 else "stream"
+                    if coll == pat.PAT_ALLGATHER:
+                        outs[fusion] = run_ag(n, count, dtype, seed, mode=mode)
+                    else:
+                        outs[fusion] = run_rs(n, count, dtype, seed + 1, mode=mode)
+                pat.check(pat.pat_set_top_fusion("auto"))
+                if coll == pat.PAT_ALLGATHER:
+                    got, host_in = outs["on"]
+                    np.testing.assert_array_equal(got, D.allgather(host_in))
+                    np.testing.assert_array_equal(got, outs["off"][0])
+                else:
+                    check_rs(outs["on"], host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+                             oracle_t(coll, n, count, dtype))
+                    np.testing.assert_array_equal(outs["on"], outs["off"])
+                ran += 1
     finally:
         pat.check(pat.pat_set_top_fusion("auto"))
+        pat.check(pat.pat_set_buffer_bytes(0))
+    assert ran > 0
 
 
 def test_workload3_and_2_with_fusion_forced_on():

@@ -323,23 +323,35 @@ def test_large_rank_counts_match_oracle(n):
 
 
 @pytest.mark.parametrize("order", ["far", "close"])
-@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 7, 8, 9, 16, 24, 33, 64, 100, 129, 1000])
-def test_full_aggregation_every_slot_serves_one_tree(n, order):
-    """At full aggregation (T = 2^(L-1), sub-trees of span 2) the linear part
-    is one distance-1 step whose receivers are leaves (all-gather) or top
-    positions (reduce-scatter), so every slot entry of the whole schedule
-    serves one tree: all steps may run as one fused launch."""
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 7, 8, 9, 12, 16, 24, 33, 64, 100, 129, 1000])
+def test_whole_schedule_slots_serve_one_tree_up_to_span_4(n, order):
+    """When the sub-trees span M <= 4 every slot entry of the whole schedule
+    serves one tree, linear part included: its distance-2 entry at index p / 4
+    is used by position 4 idx + 2 alone, and leaves use no entry.  All steps
+    may then run as one fused launch.  From span 8 on, the distance-2 entries
+    of positions 8 idx + 2 and 8 idx + 6 are shared by two trees (unless
+    truncation leaves 8 idx + 6 a leaf, as at N = 6 and 7)."""
     count = 64
     pat.check(pat.pat_set_linear_order(order))
     try:
         L = opat.ceil_log2(n)
-        pat.pat_set_buffer_bytes(budget_for(n, max(L - 1, 0), count * 4))
-        for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
-            st, info = pat.pat_plan_info(coll, n, count, "float32")
-            assert info["t"] == max(L - 1, 0)
-            _, steps, entries = library_steps(coll, n, count, "float32")
-            use = _slot_trees(coll, n, steps, entries, 0, len(steps))
-            assert all(len(trees) == 1 for trees in use.values()), coll
+        for t in range(max(L - 4, 0), max(L, 1)):
+            pat.pat_set_buffer_bytes(budget_for(n, t, count * 4))
+            for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+                st, info = pat.pat_plan_info(coll, n, count, "float32")
+                if info["t"] != t:
+                    continue  # truncation made this budget reach the next level
+                M = 1 << (L - t)
+                _, steps, entries = library_steps(coll, n, count, "float32")
+                use = _slot_trees(coll, n, steps, entries, 0, len(steps))
+                one = all(len(trees) == 1 for trees in use.values())
+                assert one == (M <= 4 or n in (6, 7)), (coll, t, M)
+                if M <= 4 and len(steps) >= 2:
+                    pat.check(pat.pat_set_top_fusion("on"))
+                    _, fused = pat.pat_plan_info(coll, n, count, "float32")
+                    pat.check(pat.pat_set_top_fusion("auto"))
+                    assert fused["fused_steps"] == len(steps) and fused["launches_per_op"] == 1
     finally:
         pat.pat_set_buffer_bytes(0)
         pat.pat_set_linear_order("far")
+        pat.check(pat.pat_set_top_fusion("auto"))
