@@ -5,6 +5,7 @@ Integer work: every comparison is exact.  No GPU needed.
 """
 
 import pytest
+from hypothesis import given, settings, strategies as hs
 
 from oracle import pat as opat
 from paper_2506_20252_amd import pat
@@ -355,3 +356,36 @@ def test_whole_schedule_slots_serve_one_tree_up_to_span_4(n, order):
         pat.pat_set_buffer_bytes(0)
         pat.pat_set_linear_order("far")
         pat.check(pat.pat_set_top_fusion("auto"))
+
+
+@settings(max_examples=60, deadline=None, derandomize=True)
+@given(n=hs.integers(min_value=2, max_value=6000), level=hs.floats(min_value=0.0, max_value=1.0),
+       order=hs.sampled_from(["far", "close"]))
+def test_random_rank_counts_match_oracle(n, level, order):
+    """Rank counts drawn over 2 .. 6000 (a fixed, derandomized draw), at an
+    aggregation level drawn over 0 .. L-1: the library's steps equal the
+    oracle's; there are t + M - 1 of them (sub-trees of span M = 2^(L-t),
+    fewer when truncation empties a step), and they move N - 1 chunks per
+    rank in all."""
+    L = opat.ceil_log2(n)
+    t = min(L - 1, int(level * L))
+    count = 4
+    pat.check(pat.pat_set_linear_order(order))
+    try:
+        pat.pat_set_buffer_bytes(budget_for(n, t, count * 4))
+        st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, count, "float32")
+        assert st == pat.PAT_OK
+        t = info["t"]  # truncation may let this budget reach the next level
+        ref = [(d, sorted(P)) for d, P in opat.schedule(n, t, order)]
+        got, steps, _ = library_steps(pat.PAT_ALLGATHER, n, count, "float32")
+        assert got == ref
+        got_rs, _, _ = library_steps(pat.PAT_REDUCESCATTER, n, count, "float32")
+        assert got_rs == ref[::-1]
+        assert sum(k for _, k in steps) == n - 1
+        assert len(steps) <= t + (1 << (L - t)) - 1
+        if n == 1 << L:
+            assert len(steps) == t + (1 << (L - t)) - 1
+    finally:
+        pat.pat_set_buffer_bytes(0)
+        pat.pat_set_linear_order("far")
+
