@@ -17,7 +17,8 @@ Prints one JSON line:
                 a bounded sample of the same workload, in the same unit
 
 python bench.py [--steps K] [--warmup W] [--mode persistent|graph|stream]
-                [--workload 1..5] [--cpu-seconds S] [--no-cpu-baseline]
+                [--workload 1..7] [--cpu-seconds S] [--no-cpu-baseline]
+(workloads 6 and 7: the all-gather in the small-size and bandwidth regimes)
 """
 
 import argparse
@@ -51,6 +52,9 @@ WORKLOADS = {
     # the all-gather of the small-size regime (workload 4's other collective)
     6: ("ag", 1000, 64, "float32", "f32_pm1", 0x5041544,
         "PAT all-gather, N=1000 virtual ranks, fp32 U[-1,1), 64-element (256 B) chunk per rank"),
+    # the all-gather in the bandwidth regime (1 MiB chunks, 16 GiB of receive buffers)
+    7: ("ag", 128, 262144, "float32", "f32_normal", 0x5041547,
+        "PAT all-gather, N=128 virtual ranks, fp32 N(0,1), 262144-element (1 MiB) chunk per rank"),
 }
 
 KERNEL_SOURCES = ["paper_2506_20252_amd/csrc/kernels.hip", "paper_2506_20252_amd/csrc/kernels.hpp",
@@ -260,8 +264,10 @@ def other_workloads(reps=50):
 def streaming_ceiling(nbytes=4 << 30, reps=10):
     """The GPU's streaming bandwidth for the step kernels' access shapes, from
     the plain probe kernels of libpatceiling.so (one 16-byte vector per lane,
-    nontemporal): a copy, and a float32 add of two buffers into a third (the
-    reduce-scatter shape).  GB/s of bytes read + written."""
+    nontemporal): a copy (an all-gather step into leaves), a copy into two
+    buffers (an all-gather step into forwarding receivers), and a float32 add
+    of two buffers into a third (the reduce-scatter shape).  GB/s of bytes
+    read + written."""
     import ctypes
 
     import torch
@@ -270,7 +276,7 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built: run __graft_entry__.build()")
     lib = ctypes.CDLL(path)
-    for name, nargs in (("pat_ceiling_copy", 2), ("pat_ceiling_add", 3)):
+    for name, nargs in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3)):
         fn = getattr(lib, name)
         fn.argtypes = [ctypes.c_void_p] * nargs + [ctypes.c_size_t, ctypes.c_void_p]
         fn.restype = ctypes.c_int
@@ -280,9 +286,12 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
     b = torch.full_like(a, 2.0)
     c = torch.empty_like(a)
     out = {"bytes_per_buffer": nbytes, "kernel": "16 B/lane, 256 lanes/workgroup, nontemporal"}
+    # the two-buffer copy runs last: it overwrites b, an input of the add
     runs = (("copy_gbps", 2, lambda: lib.pat_ceiling_copy(a.data_ptr(), c.data_ptr(), nbytes, stream.cuda_stream)),
             ("rs_shape_gbps", 3, lambda: lib.pat_ceiling_add(a.data_ptr(), b.data_ptr(), c.data_ptr(), nbytes,
-                                                             stream.cuda_stream)))
+                                                             stream.cuda_stream)),
+            ("ag_shape_gbps", 3, lambda: lib.pat_ceiling_copy2(a.data_ptr(), c.data_ptr(), b.data_ptr(), nbytes,
+                                                               stream.cuda_stream)))
     for key, streams, op in runs:
         for _ in range(2):
             if op() != 0:
@@ -295,8 +304,10 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
         e1.record(stream)
         torch.cuda.synchronize()
         out[key] = round(streams * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
-    if not bool(torch.equal(c[:1 << 20], torch.full_like(c[:1 << 20], 3.0))):
-        raise RuntimeError("ceiling probe: wrong sum")
+        if key == "rs_shape_gbps" and not bool(torch.equal(c[:1 << 20], torch.full_like(c[:1 << 20], 3.0))):
+            raise RuntimeError("ceiling probe: wrong sum")
+    if not (bool(torch.equal(b[:1 << 20], a[:1 << 20])) and bool(torch.equal(c[:1 << 20], a[:1 << 20]))):
+        raise RuntimeError("ceiling probe: wrong two-buffer copy")
     del a, b, c
     torch.cuda.empty_cache()
     return out
@@ -592,7 +603,7 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_ceiling:
         ceil = streaming_ceiling()
-        shape_key = "rs_shape_gbps" if coll == "rs" else "copy_gbps"
+        shape_key = "rs_shape_gbps" if coll == "rs" else "ag_shape_gbps"
         ceil["roofline_achieved_over_" + shape_key] = round(achieved / ceil[shape_key], 4)
         out["streaming_ceiling"] = ceil
     print(json.dumps(out), flush=True)

@@ -2,8 +2,9 @@
 
 * paper_2506_20252_amd/libpat.so -- the PAT collectives (C-ABI of include/pat.h)
 * synth/libpatsynth.so           -- the seeded input filler used by tests and the benchmark
-* paper_2506_20252_amd/libpatceiling.so -- streaming-ceiling probes (copy, 2-read/1-write add) that
-                                          the benchmark reports beside the collectives
+* paper_2506_20252_amd/libpatceiling.so -- streaming-ceiling probes (a copy, a copy into two buffers,
+                                          a 2-read/1-write add) that the benchmark reports beside
+                                          the collectives
 """
 
 import os

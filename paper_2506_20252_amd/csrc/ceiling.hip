@@ -1,7 +1,9 @@
 // Streaming ceilings of the GPU for the step kernels' access shapes, measured
-// by the benchmark beside the collectives: a copy (one read, one write) and a
-// float32 add of two streams into a third (two reads, one write, the shape of
-// a reduce-scatter step).  One 16-byte vector per lane, 256 lanes per
+// by the benchmark beside the collectives: a copy (one read, one write, the
+// shape of an all-gather step into leaves), a copy into two buffers (one
+// read, two writes, the shape of an all-gather step into forwarding
+// receivers) and a float32 add of two streams into a third (two reads, one
+// write, the shape of a reduce-scatter step).  One 16-byte vector per lane, 256 lanes per
 // workgroup, nontemporal loads and stores: the fastest form of each on
 // MI355X among 1, 2, 4 and 8 vectors per lane.  Not part of the collectives.
 #include <hip/hip_runtime.h>
@@ -22,6 +24,15 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(const v4u* src, v4u* dst
   if (i < n) {
     const v4u x = __builtin_nontemporal_load((const PAT_GLOBAL v4u*)(src + i));
     __builtin_nontemporal_store(x, (PAT_GLOBAL v4u*)(dst + i));
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void copy2_kernel(const v4u* src, v4u* dst, v4u* dst2, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) {
+    const v4u x = __builtin_nontemporal_load((const PAT_GLOBAL v4u*)(src + i));
+    __builtin_nontemporal_store(x, (PAT_GLOBAL v4u*)(dst + i));
+    __builtin_nontemporal_store(x, (PAT_GLOBAL v4u*)(dst2 + i));
   }
 }
 
@@ -49,6 +60,17 @@ extern "C" int pat_ceiling_copy(const void* src, void* dst, size_t bytes, hipStr
   if (int e = launch_check(n)) return e;
   hipLaunchKernelGGL(copy_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
                      (const v4u*)src, (v4u*)dst, n);
+  return (int)hipGetLastError();
+}
+
+// dst[0 .. bytes) = dst2[0 .. bytes) = src[0 .. bytes); same rules as the copy.
+extern "C" int pat_ceiling_copy2(const void* src, void* dst, void* dst2, size_t bytes, hipStream_t stream) {
+  if (!src || !dst || !dst2 || bytes % 16 || ((uintptr_t)src | (uintptr_t)dst | (uintptr_t)dst2) % 16)
+    return (int)hipErrorInvalidValue;
+  const int64_t n = (int64_t)(bytes / 16);
+  if (int e = launch_check(n)) return e;
+  hipLaunchKernelGGL(copy2_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
+                     (const v4u*)src, (v4u*)dst, (v4u*)dst2, n);
   return (int)hipGetLastError();
 }
 

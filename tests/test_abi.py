@@ -112,3 +112,19 @@ def test_plan_info_workloads():
         assert len(sizes) == 1
     finally:
         pat.pat_set_buffer_bytes(0)
+
+
+def test_ceiling_probe_library_exports_and_checks_arguments():
+    """The benchmark's streaming-ceiling probes (not part of the collectives)
+    load, export their three entry points, and refuse null or misaligned
+    buffers and sizes that are not whole 16-byte vectors before any launch."""
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2506_20252_amd", "libpatceiling.so"))
+    invalid = 1  # hipErrorInvalidValue
+    for name, nbuf in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3)):
+        fn = getattr(lib, name)
+        fn.argtypes = [ctypes.c_void_p] * nbuf + [ctypes.c_size_t, ctypes.c_void_p]
+        fn.restype = ctypes.c_int
+        good = [0x100000 * (i + 1) for i in range(nbuf)]
+        assert fn(*([None] + good[1:]), 4096, None) == invalid, name
+        assert fn(*(good[:-1] + [good[-1] + 8]), 4096, None) == invalid, name
+        assert fn(*good, 4100, None) == invalid, name
