@@ -215,6 +215,38 @@ def test_workload5_rs_bf16_n128_full_size(mode):
     torch.cuda.empty_cache()
 
 
+def test_workload7_ag_f32_n128_full_size():
+    """The bandwidth-regime all-gather at its benchmarked size (16 GiB of
+    receive buffers, stream mode): three whole receive buffers, and 200 000
+    sampled (rank, chunk, element) positions of the others, against the
+    definition on the host twin of the inputs."""
+    n, count, seed = 128, 262144, 0x5041547
+    log(f"[gpu] all-gather n={n} count={count} float32 seed={seed:#x} (full size)")
+    dev = torch.device("cuda:0")
+    send = torch.empty((n, count), dtype=torch.float32, device=dev)
+    fill_ranks(send, "f32_normal", seed)
+    recv = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+    recv.view(torch.uint8).fill_(0xA5)
+    pat.check(pat.pat_set_exec_mode("stream"))
+    stream = torch.cuda.current_stream()
+    pat.check(pat.pat_allgather(list(send), list(recv), count, "float32", n, stream), "ag")
+    pat.check(pat.pat_check_device_status(stream), "status")
+    host_in = np.stack([synth.host_buffer("f32_normal", seed, x, count) for x in range(n)])
+    want_bits = host_in.view(np.uint32)
+    for r in (0, 77, n - 1):
+        np.testing.assert_array_equal(as_bits(recv[r]).view(np.uint32), want_bits.reshape(-1))
+    rng = np.random.default_rng(7)
+    m = 200000
+    rr, xx, ii = rng.integers(0, n, m), rng.integers(0, n, m), rng.integers(0, count, m)
+    ii[:4] = [0, count - 1, 0, count - 1]
+    flat = torch.as_tensor(rr * (n * count) + xx * count + ii, device=dev)
+    got = as_bits(recv.view(-1)[flat]).view(np.uint32)
+    np.testing.assert_array_equal(got, want_bits[xx, ii])
+    del send, recv, flat
+    pat.check(pat.pat_finalize())
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------------------
 # Sweeps: rank counts, ragged sizes, budgets (aggregation levels, pieces), modes
 # ---------------------------------------------------------------------------
