@@ -165,6 +165,13 @@ int elem_size(pat_dtype_t t) { return t == PAT_BFLOAT16 ? 2 : 4; }
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Bytes between consecutive slot entries (and root accumulators) of a rank.
+// Entries of 256 bytes or more start on 256-byte boundaries.  Smaller ones are
+// packed at their own size: a multiple of 16 whenever the 128-bit path can
+// run, of the element size otherwise.  Padding them to 256 bytes would make
+// the intermediate memory of tiny chunks up to 64 times the data it holds.
+size_t entry_stride(size_t bytes) { return bytes >= 256 ? round_up(bytes, 256) : bytes; }
+
 #define HIP_TRY(expr)                                 \
   do {                                                \
     hipError_t e_ = (expr);                           \
@@ -313,9 +320,9 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->xcd_run = xcd_run_for(coll);
   p->alg_bytes = d.alg_bytes;
 
-  p->slot_chunk_stride = (int64_t)round_up(size_t(d.piece_elems) * d.esize_slot, 256);
+  p->slot_chunk_stride = (int64_t)entry_stride(size_t(d.piece_elems) * d.esize_slot);
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
-  if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)round_up(size_t(d.piece_elems) * 4, 256);
+  if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)entry_stride(size_t(d.piece_elems) * 4);
   p->bytes = size_t(p->slot_rank_stride + p->rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
              (p->steps[0].size() + p->steps[1].size()) * sizeof(pat::DevStep) + 2 * N * sizeof(void*) +
              pat::queue_words(std::max(p->steps[0].size(), p->steps[1].size())) * sizeof(unsigned);
@@ -674,9 +681,9 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   info.slot_elem_bytes = (size_t)d.esize_slot;
   info.slot_dims = d.slots.dims;
   info.slot_chunks_per_rank = d.slots.entries;
-  const size_t chunk_stride = round_up(size_t(d.piece_elems) * d.esize_slot, 256);
+  const size_t chunk_stride = entry_stride(size_t(d.piece_elems) * d.esize_slot);
   info.slot_bytes_per_rank = chunk_stride * d.slots.entries;
-  const size_t root = (coll == PAT_REDUCESCATTER && dtype == PAT_BFLOAT16) ? round_up(size_t(d.piece_elems) * 4, 256) : 0;
+  const size_t root = (coll == PAT_REDUCESCATTER && dtype == PAT_BFLOAT16) ? entry_stride(size_t(d.piece_elems) * 4) : 0;
   info.slot_bytes_total = (info.slot_bytes_per_rank + root) * size_t(nranks);
   info.alg_bytes = d.alg_bytes;
   info.bus_bytes_per_rank = double(nranks - 1) * double(count) * d.esize_in;

@@ -22,6 +22,7 @@ import pytest
 import torch
 
 import synth
+from closed_forms import tree_sum
 from oracle import definitions as D
 from oracle import pat as opat
 from paper_2506_20252_amd import pat
@@ -245,6 +246,66 @@ def test_workload7_ag_f32_n128_full_size():
     del send, recv, flat
     pat.check(pat.pat_finalize())
     torch.cuda.empty_cache()
+
+
+def test_maximum_rank_count():
+    """N = 65536, the largest rank count the library accepts, with one-element
+    chunks (16 GiB of rank buffers per collective, 128 KiB of slots per rank,
+    16 steps).  The oracle's executors are quadratic in N, so outputs are
+    sampled: the all-gather at 200 000 (receiver, chunk) pairs against the
+    definition; the reduce-scatter at 48 destination ranks, int32 against the
+    wrapped plain sum and float32 bit-exact against the closed form of the
+    reversed trees (pinned to the oracle on small N) and within 1e-5 of the
+    plain sum."""
+    n, seed = 65536, 0x6A55
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode("stream"))
+    stream = torch.cuda.current_stream()
+    rng = np.random.default_rng(11)
+
+    log(f"[gpu] all-gather n={n} count=1 int32 seed={seed:#x} (maximum rank count)")
+    send = torch.empty((n, 1), dtype=torch.int32, device=dev)
+    fill_ranks(send, "int32_pm2p20", seed)
+    recv = torch.empty((n, n), dtype=torch.int32, device=dev)
+    recv.view(torch.uint8).fill_(0xA5)
+    pat.check(pat.pat_allgather(list(send), list(recv), 1, "int32", n, stream), "ag")
+    pat.check(pat.pat_check_device_status(stream), "status")
+    xs = np.unique(np.concatenate([[0, 1, n - 1], rng.integers(0, n, 2000)]))
+    want = {int(x): synth.host_values("int32_pm2p20", seed, int(x), np.zeros(1, dtype=np.uint64))[0] for x in xs}
+    xx = rng.choice(xs, 200000)
+    rr = rng.integers(0, n, 200000)
+    got = recv.view(-1)[torch.as_tensor(rr * n + xx, device=dev)].cpu().numpy()
+    np.testing.assert_array_equal(got, np.array([want[int(x)] for x in xx], dtype=np.int32))
+    del send, recv
+    pat.check(pat.pat_finalize())
+    torch.cuda.empty_cache()
+
+    R = np.unique(np.concatenate([[0, 1, n - 1], rng.integers(0, n, 45)]))
+    q = np.arange(n)
+    for dtype, dist in (("int32", "int32_pm2p20"), ("float32", "f32_normal")):
+        log(f"[gpu] reduce-scatter n={n} count=1 {dtype} seed={seed:#x} (maximum rank count)")
+        send = torch.empty((n, n), dtype=TORCH[dtype], device=dev)
+        fill_ranks(send, dist, seed)
+        out = torch.empty((n, 1), dtype=TORCH[dtype], device=dev)
+        pat.check(pat.pat_reducescatter(list(send), list(out), 1, dtype, pat.PAT_SUM, n, stream), "rs")
+        pat.check(pat.pat_check_device_status(stream), "status")
+        got = as_bits(out[torch.as_tensor(R, device=dev), 0])
+        # vals[x, k]: rank x's contribution to destination R[k]
+        vals = np.stack([synth.host_values(dist, seed, x, R.astype(np.uint64)) for x in range(n)])
+        if dtype == "int32":
+            want = (vals.astype(np.int64).sum(axis=0) & 0xFFFFFFFF).astype(np.uint32).view(np.int32)
+            np.testing.assert_array_equal(got, want)
+        else:
+            # tree position q of destination R is rank R + q
+            v = vals[(R[None, :] + q[:, None]) % n, np.arange(len(R))[None, :]]
+            want = tree_sum(v, n)
+            np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+            exact = vals.astype(np.float64).sum(axis=0)
+            scale = np.abs(vals.astype(np.float64)).sum(axis=0)
+            assert (np.abs(got.astype(np.float64) - exact) <= 1e-5 * scale).all()
+        del send, out
+        pat.check(pat.pat_finalize())
+        torch.cuda.empty_cache()
 
 
 # ---------------------------------------------------------------------------

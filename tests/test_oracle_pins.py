@@ -17,6 +17,7 @@ import math
 import numpy as np
 import pytest
 
+from closed_forms import tree_sum
 from conftest import read_golden
 from oracle import bruck, pat
 from oracle import definitions as D
@@ -202,23 +203,6 @@ def test_aggregation_level_fits_budget():
 # --------------------------------------------------------------------------
 # Brute force on tiny N; closed form of the reversed-tree association
 # --------------------------------------------------------------------------
-
-def tree_sum(v, n):
-    """Reversed binomial tree, nearest child first, written from the tree:
-    the node at `lo` owning span w first sums its own half-span, then adds the
-    partial of the child at lo + w/2 (absent if truncated).  float32 adds."""
-    L = pat.ceil_log2(n)
-
-    def S(lo, w):
-        if w == 1:
-            return v[lo]
-        left = S(lo, w // 2)
-        if lo + w // 2 >= n:
-            return left
-        return (left + S(lo + w // 2, w // 2)).astype(np.float32)
-
-    return S(0, 1 << L)
-
 
 def closed_form(inputs, dtype):
     n = inputs.shape[0]

@@ -389,3 +389,28 @@ def test_random_rank_counts_match_oracle(n, level, order):
         pat.pat_set_buffer_bytes(0)
         pat.pat_set_linear_order("far")
 
+
+
+@pytest.mark.parametrize("n,count,dtype,coll", [(65536, 1, "float32", pat.PAT_REDUCESCATTER),
+                                                (65536, 1, "int32", pat.PAT_ALLGATHER),
+                                                (1000, 64, "float32", pat.PAT_REDUCESCATTER),
+                                                (24, 17, "bfloat16", pat.PAT_REDUCESCATTER),
+                                                (128, 2 << 20, "bfloat16", pat.PAT_REDUCESCATTER)])
+def test_slot_memory_follows_the_data(n, count, dtype, coll):
+    """Intermediate memory per rank is the slot entries times the entry's own
+    size when an entry is under 256 bytes (packed), else times its size
+    rounded up to 256 bytes; bf16 reduce-scatters add one float32 root
+    accumulator per rank.  At N = 65536 with one-element chunks that is 128 KiB
+    per rank, not 32767 entries padded to 256 bytes (512 GiB in all)."""
+    st, info = pat.pat_plan_info(coll, n, count, dtype)
+    assert st == pat.PAT_OK
+    entry = info["piece_elems"] * info["slot_elem_bytes"]
+    stride = entry if entry < 256 else -(-entry // 256) * 256
+    assert info["slot_bytes_per_rank"] == info["slot_chunks_per_rank"] * stride
+    root = 0
+    if coll == pat.PAT_REDUCESCATTER and dtype == "bfloat16":
+        root_entry = info["piece_elems"] * 4
+        root = root_entry if root_entry < 256 else -(-root_entry // 256) * 256
+    assert info["slot_bytes_total"] == (info["slot_bytes_per_rank"] + root) * n
+    if n == 65536:
+        assert info["slot_bytes_per_rank"] == 32767 * 4
