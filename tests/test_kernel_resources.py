@@ -54,3 +54,16 @@ def test_no_kernel_uses_scratch(device_asm):
 
 def test_no_packed_fp32(device_asm):
     assert not re.search(r"\bv_pk_(add|mul|fma)_f32\b", device_asm)
+
+
+def test_fused_kernel_keeps_five_workgroups_per_cu(device_asm):
+    """The fused kernel's tile choice keeps its grid at <= 1024 workgroups,
+    assuming every variant holds at least 5 workgroups of 256 lanes per CU
+    (1280 on 256 CUs) at once: 512 VGPRs per SIMD lane, in granules of 8,
+    leave room for 5 waves per SIMD up to 96 VGPRs (plus accumulation
+    registers, of which these kernels use none)."""
+    ks = [(n, v) for n, _, v in kernels(device_asm) if "tree_kernel" in n]
+    assert len(ks) >= 18
+    bad = [(n, v) for n, v in ks if (v + 7) // 8 * 8 > 96]
+    assert not bad, bad
+    assert not re.search(r"\bv_accvgpr", device_asm)
