@@ -160,11 +160,12 @@ int pat_get_exec_mode(void);
  * tree's steps one after another, so wide steps (many chunks per rank) are
  * better left to one kernel each.  AUTO (the default, or the PAT_TOP_FUSION
  * environment variable: auto | on | off) fuses the far end of the fusable
- * range, the steps that move at most 64 MiB and in which one tree's edges
- * over one tile of its chunk (256 vectors) amount to at most 2048 vectors,
- * when there are two or more such steps; ON fuses the whole fusable range
- * whenever it has two or more steps.  Neither fuses a chunk that is split
- * into pieces.
+ * range, the steps that move at most 128 MiB (reduce-scatter) or 64 MiB
+ * (all-gather) and in which one tree's edges over one tile of its chunk
+ * amount to at most 2048 vectors, when there are two or more such steps; ON
+ * fuses the whole fusable range whenever it has two or more steps.  Neither
+ * fuses a chunk that is split into pieces.  A tile is the smallest power of
+ * two from 32 to 256 vectors that keeps the launch within 1024 workgroups.
  */
 typedef enum { PAT_FUSION_AUTO = 0, PAT_FUSION_OFF = 1, PAT_FUSION_ON = 2 } pat_fusion_t;
 pat_status_t pat_set_top_fusion(int mode);
