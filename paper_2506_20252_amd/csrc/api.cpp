@@ -437,6 +437,18 @@ bool overlaps_ok(int coll, const void* const* send, void* const* recv, int N, si
   return true;
 }
 
+// The pointer set a thread last passed the per-pointer checks with, and what
+// they found.  A caller that reuses its buffers passes the same set call after
+// call; comparing it costs O(N) instead of the checks' O(N log N).
+struct CheckedPointers {
+  int coll = -1, N = 0, dt = -1;
+  size_t count = 0;
+  std::vector<const void*> send;
+  std::vector<void*> recv;
+  bool vec = false;
+};
+thread_local CheckedPointers t_checked;
+
 pat_status_t run(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt, int N,
                  hipStream_t stream) {
   if (N < 1 || N > kMaxRanks || send == nullptr || recv == nullptr) return PAT_ERR_INVALID_ARGUMENT;
@@ -445,16 +457,31 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   if (count > (size_t(1) << 40) / es || (unsigned __int128)count * es * N > ((unsigned __int128)1 << 62))
     return PAT_ERR_INVALID_ARGUMENT;
   if (count == 0) return PAT_OK;
-  bool vec = true;
-  for (int r = 0; r < N; ++r) {
-    if (!send[r] || !recv[r]) return PAT_ERR_INVALID_ARGUMENT;
-    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % es) return PAT_ERR_INVALID_ARGUMENT;
-    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % 16) vec = false;
-  }
   const size_t chunk = count * es;
-  const size_t send_bytes = coll == 0 ? chunk : chunk * N;
-  const size_t recv_bytes = coll == 0 ? chunk * N : chunk;
-  if (!overlaps_ok(coll, send, recv, N, send_bytes, recv_bytes, chunk)) return PAT_ERR_INVALID_ARGUMENT;
+  CheckedPointers& ck = t_checked;
+  const bool checked = ck.coll == coll && ck.N == N && ck.dt == (int)dt && ck.count == count &&
+                       !std::memcmp(ck.send.data(), send, N * sizeof(void*)) &&
+                       !std::memcmp(ck.recv.data(), recv, N * sizeof(void*));
+  bool vec = ck.vec;
+  if (!checked) {
+    ck.coll = -1;  // invalid until this set passes
+    vec = true;
+    for (int r = 0; r < N; ++r) {
+      if (!send[r] || !recv[r]) return PAT_ERR_INVALID_ARGUMENT;
+      if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % es) return PAT_ERR_INVALID_ARGUMENT;
+      if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % 16) vec = false;
+    }
+    const size_t send_bytes = coll == 0 ? chunk : chunk * N;
+    const size_t recv_bytes = coll == 0 ? chunk * N : chunk;
+    if (!overlaps_ok(coll, send, recv, N, send_bytes, recv_bytes, chunk)) return PAT_ERR_INVALID_ARGUMENT;
+    ck.send.assign(send, send + N);
+    ck.recv.assign(recv, recv + N);
+    ck.N = N;
+    ck.dt = (int)dt;
+    ck.count = count;
+    ck.vec = vec;
+    ck.coll = coll;
+  }
 
   if (N == 1) {
     if (send[0] != recv[0])
@@ -483,19 +510,23 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     for (int r = 0; r < N && !own_copy; ++r)
       own_copy = (const char*)send[r] != (const char*)recv[r] + size_t(r) * chunk;
 
-  // Pointer tables: upload only when they changed since the last call.
-  bool same = plan->h_send.size() == size_t(N);
-  for (int r = 0; r < N && same; ++r) same = plan->h_send[r] == send[r] && plan->h_recv[r] == recv[r];
+  // Pointer tables: upload only when they changed since the last call.  The
+  // remembered set is replaced only once its upload is queued.
+  const bool same = plan->h_send.size() == size_t(N) &&
+                    !std::memcmp(plan->h_send.data(), send, N * sizeof(void*)) &&
+                    !std::memcmp(plan->h_recv.data(), recv, N * sizeof(void*));
   if (!same) {
     if (plan->upload_pending) HIP_TRY(hipEventSynchronize(plan->upload_done));
-    plan->h_send.assign(send, send + N);
-    plan->h_recv.assign(recv, recv + N);
+    plan->h_send.clear();
+    plan->h_recv.clear();
     std::memcpy(plan->pinned, send, N * sizeof(void*));
     std::memcpy(plan->pinned + N, recv, N * sizeof(void*));
     HIP_TRY(hipMemcpyAsync(plan->d_send, plan->pinned, N * sizeof(void*), hipMemcpyHostToDevice, stream));
     HIP_TRY(hipMemcpyAsync(plan->d_recv, plan->pinned + N, N * sizeof(void*), hipMemcpyHostToDevice, stream));
     HIP_TRY(hipEventRecord(plan->upload_done, stream));
     plan->upload_pending = true;
+    plan->h_send.assign(send, send + N);
+    plan->h_recv.assign(recv, recv + N);
   }
 
   const pat::PlanDesc& d = plan->desc;

@@ -601,6 +601,37 @@ def test_graph_mode_follows_fusion_changes_on_one_plan():
     assert (np.abs(outs[0].astype(np.float64) - exact) <= 1e-5 * scale).all()
 
 
+def test_pointer_checks_follow_every_argument():
+    """The per-pointer checks are skipped only for the exact pointer set a
+    thread last validated with the same operation, rank count, count and
+    dtype.  The same receive pointers with a doubled count overlap (rows are
+    packed for the smaller count) and must be refused before any launch; the
+    valid call still works before and after, and a one-entry change is
+    checked again."""
+    n, count, seed = 4, 64, 0x5EC
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode("stream"))
+    stream = torch.cuda.current_stream()
+    send = torch.empty((n, 2 * count), dtype=torch.float32, device=dev)
+    fill_ranks(send, "f32_normal", seed)
+    recv = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+    S, R = pat.pointer_array([send[x, :count] for x in range(n)]), pat.pointer_array(list(recv))
+    want = np.stack([synth.host_buffer("f32_normal", seed, x, 2 * count)[:count] for x in range(n)])
+    for attempt in range(2):
+        for repeat in range(2):  # the second call takes the already-checked path
+            recv.fill_(-1.0)
+            pat.check(pat.pat_allgather(S, R, count, "float32", n, stream), "ag")
+            got = as_bits(recv).reshape(n, n, count)
+            for r in range(n):
+                np.testing.assert_array_equal(got[r], want)
+        # doubled count: receive rows of n * 2 * count elements overlap their neighbours
+        assert pat.pat_allgather(S, R, 2 * count, "float32", n, stream) == pat.PAT_ERR_INVALID_ARGUMENT
+        # a set that differs in one entry (rank 1's receive buffer inside rank 0's) is checked again
+        bad = pat.pointer_array([recv[0].data_ptr()] + [recv[0].data_ptr() + 256] + [recv[r].data_ptr() for r in (2, 3)])
+        assert pat.pat_allgather(S, bad, count, "float32", n, stream) == pat.PAT_ERR_INVALID_ARGUMENT
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
 def test_caller_created_stream(mode):
     """The collectives run on the stream they are given, not only on the
