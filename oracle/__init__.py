@@ -23,7 +23,10 @@ Contents (all plain, slow and written to be checked against the paper by eye):
   "The PAT algorithm" and "Conversion to reduce-scatter operations".
 
 Parity status: every function here is pinned by tests in
-``tests/test_oracle_pins.py`` except the choice of fp32 association for the
-reduce-scatter, which the paper never prints; see ``pat.reducescatter`` for
-the reading it follows ("parity unpinned" beyond that reading).
+``tests/test_oracle_pins.py``.  The reduce-scatter's float32 association is
+pinned to the reversed-tree closed form written in the tests from the tree
+definition, to its invariance across aggregation levels and to the pairwise
+error bound; which association the paper intends is a reading (the paper
+prints no values), listed with the others in the design notes, and the
+tolerance check against the fp64 plain sum does not depend on it.
 """
