@@ -72,13 +72,13 @@ def host_rs_inputs(n, count, dist, seed, sample=None):
     return np.stack([synth.host_values(dist, seed, x, idx.ravel()).reshape(n, len(sample)) for x in range(n)])
 
 
-def check_rs(got, host_in, dtype, budget_t):
+def check_rs(got, host_in, dtype, budget_t, order="far"):
     """got: (N, m) from the device; host_in: (N, N, m)."""
     if dtype == "int32":
         ref = D.reducescatter_sum(host_in, "int32")
         np.testing.assert_array_equal(got, ref)
         return
-    pat_ref, _ = opat.reducescatter(host_in, budget_t, dtype)
+    pat_ref, _ = opat.reducescatter(host_in, budget_t, dtype, order)
     width = np.uint32 if dtype == "float32" else np.uint16
     mism = np.count_nonzero(got.view(width) != pat_ref.view(width))
     assert mism == 0, f"{mism} elements differ from the PAT-order oracle"
@@ -630,6 +630,45 @@ def test_pointer_checks_follow_every_argument():
         bad = pat.pointer_array([recv[0].data_ptr()] + [recv[0].data_ptr() + 256] + [recv[r].data_ptr() for r in (2, 3)])
         assert pat.pat_allgather(S, bad, count, "float32", n, stream) == pat.PAT_ERR_INVALID_ARGUMENT
     torch.cuda.synchronize()
+
+
+def _random_cases(k=40, seed=2026):
+    """A fixed, seeded draw of configurations mixing every setting."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(k):
+        n = int(rng.choice([2, 3, 5, 7, 12, 17, 31, 45, 64, 100, 129, 200]))
+        dtype = str(rng.choice(["int32", "float32", "bfloat16"]))
+        count = int(rng.choice([1, 3, 8, 33, 250, 1000, 2052]))
+        budget = int(rng.choice([0, 64, 512, 4096, 65536]))  # 0: default; small budgets force pieces
+        mode = str(rng.choice(["stream", "graph", "persistent"]))
+        fusion = str(rng.choice(["auto", "on", "off"]))
+        order = str(rng.choice(["far", "close"]))
+        coll = str(rng.choice(["ag", "rs"]))
+        cases.append((coll, n, count, dtype, budget, mode, fusion, order, int(rng.integers(1, 1 << 30))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: "-".join(str(x) for x in c[:8]))
+def test_random_configurations(case):
+    """Seeded random mixes of rank count, size, dtype, buffer budget (pieces
+    included), execution mode, fusion and linear order, against the oracle."""
+    coll, n, count, dtype, budget, mode, fusion, order, seed = case
+    pat.check(pat.pat_set_buffer_bytes(budget))
+    pat.check(pat.pat_set_top_fusion(fusion))
+    pat.check(pat.pat_set_linear_order(order))
+    try:
+        if coll == "ag":
+            got, host_in = run_ag(n, count, dtype, seed, mode=mode)
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+        else:
+            got = run_rs(n, count, dtype, seed, mode=mode)
+            check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed), dtype,
+                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype), order)
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+        pat.check(pat.pat_set_top_fusion("auto"))
+        pat.check(pat.pat_set_linear_order("far"))
 
 
 @pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
