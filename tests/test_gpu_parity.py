@@ -632,7 +632,7 @@ def test_pointer_checks_follow_every_argument():
     torch.cuda.synchronize()
 
 
-def _random_cases(k=40, seed=2026):
+def _random_cases(k=100, seed=2026):
     """A fixed, seeded draw of configurations mixing every setting."""
     rng = np.random.default_rng(seed)
     cases = []
