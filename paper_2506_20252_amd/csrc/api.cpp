@@ -730,7 +730,8 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   info.slot_chunks_per_rank = d.slots.entries;
   const size_t chunk_stride = entry_stride(size_t(d.piece_elems) * d.esize_slot);
   info.slot_bytes_per_rank = chunk_stride * d.slots.entries;
-  const size_t root = (coll == PAT_REDUCESCATTER && dtype == PAT_BFLOAT16) ? entry_stride(size_t(d.piece_elems) * 4) : 0;
+  const bool bf16_rs = coll == PAT_REDUCESCATTER && dtype == PAT_BFLOAT16;
+  const size_t root = bf16_rs ? entry_stride(size_t(d.piece_elems) * 4) : 0;
   info.slot_bytes_total = (info.slot_bytes_per_rank + root) * size_t(nranks);
   info.alg_bytes = d.alg_bytes;
   info.bus_bytes_per_rank = double(nranks - 1) * double(count) * d.esize_in;

@@ -128,9 +128,10 @@ __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int*
   *i = (int)(e - (int64_t)(*r) * st.k);
 }
 
-// Workgroup size of a fused range of steps.  A tree's steps run one after another
-// inside its workgroup, so a wide workgroup covers a whole step in fewer load
-// rounds (a shorter chain of dependent accesses per step).
+// Workgroup size of a fused range of steps.  A tree's steps run one after
+// another inside its workgroup, so a wide workgroup covers a whole step in
+// fewer load rounds (a shorter chain of dependent accesses per step).  The
+// host's tile choice assumes 256 lanes.
 #ifndef PAT_TREE_THREADS
 #define PAT_TREE_THREADS 256
 #endif
