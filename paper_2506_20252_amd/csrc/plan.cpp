@@ -12,12 +12,6 @@ int ceil_log2(int64_t n) {
   return L;
 }
 
-static int log2_exact(int64_t v) {
-  int l = 0;
-  while ((int64_t(1) << l) < v) ++l;
-  return l;
-}
-
 // Far-first pre-order walk of a full sub-tree of span `span`: from a node, the
 // farthest child first, and that child's whole sub-tree before the next, closer
 // child.  An explicit stack holds "edge (q, d) still to emit".
@@ -93,7 +87,7 @@ static bool needs_slot(int N, int p) {
 int32_t SlotMap::index(int p) const {
   if (!needs_slot(N, p)) return -1;
   const int D = p & -p;
-  return base[log2_exact(D)] + p / std::max(2 * D, M);
+  return base[ceil_log2(D)] + p / std::max(2 * D, M);
 }
 
 SlotMap make_slot_map(int N, int L, int M) {
@@ -106,7 +100,7 @@ SlotMap make_slot_map(int N, int L, int M) {
   for (int p = 1; p < N; ++p) {
     if (!needs_slot(N, p)) continue;
     const int D = p & -p;
-    const int l = log2_exact(D);
+    const int l = ceil_log2(D);
     m.cap[l] = std::max(m.cap[l], p / std::max(2 * D, M) + 1);
   }
   int32_t acc = 0;
