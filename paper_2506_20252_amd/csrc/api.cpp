@@ -282,7 +282,10 @@ void make_room(int device, size_t need) {
 }
 
 // Launch-level steps for one vector width: every schedule step of every piece.
-bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, std::vector<pat::DevStep>* out) {
+// Chunk-pieces of at least `pack_tile` vectors are split into tiled work items
+// of `tile` vectors (the last one ragged), smaller ones packed `pack_tile`
+// vectors per work item.
+bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, std::vector<pat::DevStep>* out) {
   out->clear();
   for (int piece = 0; piece < d.pieces; ++piece) {
     const int64_t e0 = int64_t(piece) * d.piece_elems;
@@ -300,12 +303,12 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, std::vector<pat
       ds.e0 = e0;
       ds.V = V;
       const int64_t edges = int64_t(d.N) * st.k;
-      if (V >= tile) {
+      if (V >= pack_tile) {
         ds.tiles_per_edge = (V + tile - 1) / tile;
         ds.items = edges * ds.tiles_per_edge;
       } else {
         ds.tiles_per_edge = 0;
-        ds.items = (edges * V + tile - 1) / tile;
+        ds.items = (edges * V + pack_tile - 1) / pack_tile;
       }
       out->push_back(ds);
     }
@@ -330,8 +333,10 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->device = device;
   const bool vec_ok = (count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
   const pat::Variant vs = variant_for(coll, dt, false), vv = variant_for(coll, dt, true);
-  if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), &p->steps[0])) return PAT_ERR_INTERNAL;
-  p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), &p->steps[1]);
+  if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), pat::variant_pack_tile(vs), &p->steps[0]))
+    return PAT_ERR_INTERNAL;
+  p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), pat::variant_pack_tile(vv),
+                                     &p->steps[1]);
   p->streaming = streaming_for(d.alg_bytes);
   p->xcd_run = xcd_run_for(coll);
   p->alg_bytes = d.alg_bytes;

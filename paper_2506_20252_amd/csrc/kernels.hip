@@ -56,6 +56,15 @@
 #ifndef PAT_B16_UNROLL
 #define PAT_B16_UNROLL (2 * PAT_UNROLL)
 #endif
+// Element-wide kernels (pointers or sizes that rule out 128-bit vectors): 4
+// elements per lane on the packed and fused paths, 8 on the tiled path, where
+// a lane's few bytes in flight otherwise limit a bandwidth-bound step.
+#ifndef PAT_SCALAR_UNROLL
+#define PAT_SCALAR_UNROLL 4
+#endif
+#ifndef PAT_SCALAR_TILED_UNROLL
+#define PAT_SCALAR_TILED_UNROLL 8
+#endif
 
 namespace pat {
 namespace {
@@ -65,6 +74,9 @@ namespace {
 typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kSU = PAT_SCALAR_UNROLL;         // element-wide kernels: packed and fused paths
+constexpr int kSTU = PAT_SCALAR_TILED_UNROLL;  // element-wide kernels: tiled path
 
 // Buffer addresses come from pointer tables, so the compiler cannot tell they
 // are global memory and would emit flat accesses; every data access goes
@@ -168,10 +180,13 @@ __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st
 // All-gather
 // ---------------------------------------------------------------------------
 
-template <typename Unit, int kU, bool NT>
+// U vectors per lane on the packed and fused paths, TU on the tiled path.
+template <typename Unit, int kU, bool NT, int kTU = kU>
 struct AgOp {
   static constexpr int U = kU;
-  static constexpr int kTile = kThreads * U;
+  static constexpr int TU = kTU;
+  static constexpr int kTile = kThreads * TU;      // vectors of one tiled work item
+  static constexpr int kPackTile = kThreads * U;   // vectors of one packed work item
 
   struct Edge {
     const char* src;
@@ -210,8 +225,8 @@ struct AgOp {
   }
 
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
-    Unit x[U];
     if (st.tiles_per_edge > 0) {
+      Unit x[TU];
       int r, i;
       int64_t tile;
       split_tile(item, st, &r, &i, &tile);
@@ -221,27 +236,27 @@ struct AgOp {
         // Full tile (uniform): straight-line loads, then one store loop per
         // destination, so no store waits for another store.
 #pragma unroll
-        for (int j = 0; j < U; ++j) x[j] = ldg<Unit, NT>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
+        for (int j = 0; j < TU; ++j) x[j] = ldg<Unit, NT>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         if (e.dst2) {
 #pragma unroll
-          for (int j = 0; j < U; ++j) stg<NT>(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < TU; ++j) stg<NT>(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         if (e.dst3) {
 #pragma unroll
-          for (int j = 0; j < U; ++j) stg<NT>(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < TU; ++j) stg<NT>(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         return;
       }
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
+      for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
         if (v < st.V) x[j] = ldg<Unit, NT>(e.src + v * (int64_t)sizeof(Unit));
       }
       wait_loads();
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
+      for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
         if (v < st.V) put(e, v, x[j]);
       }
@@ -252,7 +267,7 @@ struct AgOp {
       int64_t vv[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
-        const int64_t g = item * kTile + j * kThreads + threadIdx.x;
+        const int64_t g = item * kPackTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
         if (g < units) split_flat(g, st, &rr[j], &ii[j], &vv[j], small);
       }
@@ -312,6 +327,7 @@ struct TI32V {
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
+  static constexpr int kTiledUnroll = kUnroll;
   __device__ static acc_t widen(const in_t& x) { return x; }
   __device__ static in_t narrow(const acc_t& x) { return x; }
   __device__ static acc_t add(const acc_t& a, const acc_t& b) { return a + b; }  // wraps
@@ -323,6 +339,7 @@ struct TF32V {
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
+  static constexpr int kTiledUnroll = kUnroll;
   __device__ static acc_t widen(const in_t& x) { return x; }
   __device__ static in_t narrow(const acc_t& x) { return x; }
   __device__ static acc_t add(const acc_t& a, const acc_t& b) { return a + b; }
@@ -334,6 +351,7 @@ struct TB16V {
   static constexpr int kInElem = 2;
   static constexpr bool kSeparateRoot = true;
   static constexpr int kUnroll = PAT_B16_UNROLL;
+  static constexpr int kTiledUnroll = kUnroll;
   __device__ static acc_t widen(const in_t& x) {
     return v4f{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)};
   }
@@ -348,7 +366,8 @@ struct TI32S {
   using acc_t = uint32_t;
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
-  static constexpr int kUnroll = 4;
+  static constexpr int kUnroll = PAT_SCALAR_UNROLL;
+  static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
   __device__ static acc_t widen(in_t x) { return x; }
   __device__ static in_t narrow(acc_t x) { return x; }
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
@@ -359,7 +378,8 @@ struct TF32S {
   using acc_t = float;
   static constexpr int kInElem = 4;
   static constexpr bool kSeparateRoot = false;
-  static constexpr int kUnroll = 4;
+  static constexpr int kUnroll = PAT_SCALAR_UNROLL;
+  static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
   __device__ static acc_t widen(in_t x) { return x; }
   __device__ static in_t narrow(acc_t x) { return x; }
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
@@ -370,7 +390,8 @@ struct TB16S {
   using acc_t = float;
   static constexpr int kInElem = 2;
   static constexpr bool kSeparateRoot = true;
-  static constexpr int kUnroll = 4;
+  static constexpr int kUnroll = PAT_SCALAR_UNROLL;
+  static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
   __device__ static acc_t widen(in_t x) { return __uint_as_float((uint32_t)x << 16); }
   __device__ static in_t narrow(acc_t x) { return (uint16_t)bf16_rne(x); }
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
@@ -380,8 +401,10 @@ template <class R, bool NT>
 struct RsOp {
   using in_t = typename R::in_t;
   using acc_t = typename R::acc_t;
-  static constexpr int U = R::kUnroll;
-  static constexpr int kTile = kThreads * U;
+  static constexpr int U = R::kUnroll;         // packed and fused paths
+  static constexpr int TU = R::kTiledUnroll;   // tiled path
+  static constexpr int kTile = kThreads * TU;
+  static constexpr int kPackTile = kThreads * U;
 
   struct Edge {
     const char* child;
@@ -443,43 +466,43 @@ struct RsOp {
   // input widened right after its load would wait for each load in turn).
   template <bool OWN_RAW, bool CHILD_RAW>
   __device__ static void tile(const Edge& e, int64_t tile_idx, int64_t V) {
-    vec_t<OWN_RAW> a[U];
-    vec_t<CHILD_RAW> b[U];
+    vec_t<OWN_RAW> a[TU];
+    vec_t<CHILD_RAW> b[TU];
     const int64_t v0 = tile_idx * kTile + threadIdx.x;
     if ((tile_idx + 1) * kTile <= V) {
       // Full tile (uniform): straight-line code, no per-lane guards.
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
+      for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
         a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
         b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
-      acc_t sum[U];
+      acc_t sum[TU];
 #pragma unroll
-      for (int j = 0; j < U; ++j) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
+      for (int j = 0; j < TU; ++j) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
       if (R::kSeparateRoot && e.dst_final) {
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
+        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
       } else {
 #pragma unroll
-        for (int j = 0; j < U; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
+        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
       }
       return;
     }
 #pragma unroll
-    for (int j = 0; j < U; ++j) {
+    for (int j = 0; j < TU; ++j) {
       const int64_t v = v0 + j * kThreads;
       if (v < V) {
         a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
         b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
     }
-    acc_t sum[U];
+    acc_t sum[TU];
 #pragma unroll
-    for (int j = 0; j < U; ++j)
+    for (int j = 0; j < TU; ++j)
       if (v0 + j * kThreads < V) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
 #pragma unroll
-    for (int j = 0; j < U; ++j) {
+    for (int j = 0; j < TU; ++j) {
       const int64_t v = v0 + j * kThreads;
       if (v < V) store(e, v, sum[j]);
     }
@@ -511,7 +534,7 @@ struct RsOp {
       int64_t vv[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
-        const int64_t g = item * kTile + j * kThreads + threadIdx.x;
+        const int64_t g = item * kPackTile + j * kThreads + threadIdx.x;
         vv[j] = -1;
         if (g < units) split_flat(g, st, &rr[j], &ii[j], &vv[j], small);
       }
@@ -842,8 +865,8 @@ hipError_t capacity_t(int* blocks) {
 #define PAT_DISPATCH(v, NT, CALL)                                           \
   switch (v) {                                                              \
     case kAgVec: return NT ? CALL((AgOp<v4u, PAT_UNROLL, true>)) : CALL((AgOp<v4u, PAT_UNROLL, false>)); \
-    case kAgS4: return NT ? CALL((AgOp<uint32_t, 4, true>)) : CALL((AgOp<uint32_t, 4, false>));         \
-    case kAgS2: return NT ? CALL((AgOp<uint16_t, 4, true>)) : CALL((AgOp<uint16_t, 4, false>));         \
+    case kAgS4: return NT ? CALL((AgOp<uint32_t, kSU, true, kSTU>)) : CALL((AgOp<uint32_t, kSU, false, kSTU>)); \
+    case kAgS2: return NT ? CALL((AgOp<uint16_t, kSU, true, kSTU>)) : CALL((AgOp<uint16_t, kSU, false, kSTU>)); \
     case kRsI32Vec: return NT ? CALL((RsOp<TI32V, true>)) : CALL((RsOp<TI32V, false>));                  \
     case kRsF32Vec: return NT ? CALL((RsOp<TF32V, true>)) : CALL((RsOp<TF32V, false>));                  \
     case kRsB16Vec: return NT ? CALL((RsOp<TB16V, true>)) : CALL((RsOp<TB16V, false>));                  \
@@ -873,14 +896,29 @@ int variant_in_bytes(Variant v) {
 int variant_tile(Variant v) {
   switch (v) {
     case kAgVec: return AgOp<v4u, PAT_UNROLL, true>::kTile;
-    case kAgS4: return AgOp<uint32_t, 4, true>::kTile;
-    case kAgS2: return AgOp<uint16_t, 4, true>::kTile;
+    case kAgS4: return AgOp<uint32_t, kSU, true, kSTU>::kTile;
+    case kAgS2: return AgOp<uint16_t, kSU, true, kSTU>::kTile;
     case kRsI32Vec: return RsOp<TI32V, true>::kTile;
     case kRsF32Vec: return RsOp<TF32V, true>::kTile;
     case kRsB16Vec: return RsOp<TB16V, true>::kTile;
     case kRsI32S: return RsOp<TI32S, true>::kTile;
     case kRsF32S: return RsOp<TF32S, true>::kTile;
     case kRsB16S: return RsOp<TB16S, true>::kTile;
+    default: return 0;
+  }
+}
+
+int variant_pack_tile(Variant v) {
+  switch (v) {
+    case kAgVec: return AgOp<v4u, PAT_UNROLL, true>::kPackTile;
+    case kAgS4: return AgOp<uint32_t, kSU, true, kSTU>::kPackTile;
+    case kAgS2: return AgOp<uint16_t, kSU, true, kSTU>::kPackTile;
+    case kRsI32Vec: return RsOp<TI32V, true>::kPackTile;
+    case kRsF32Vec: return RsOp<TF32V, true>::kPackTile;
+    case kRsB16Vec: return RsOp<TB16V, true>::kPackTile;
+    case kRsI32S: return RsOp<TI32S, true>::kPackTile;
+    case kRsF32S: return RsOp<TF32S, true>::kPackTile;
+    case kRsB16S: return RsOp<TB16S, true>::kPackTile;
     default: return 0;
   }
 }

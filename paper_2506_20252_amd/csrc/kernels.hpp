@@ -54,9 +54,12 @@ enum Variant : int {
   kNumVariants
 };
 
-// Bytes of user data per vector, and vectors per work-item tile.
+// Bytes of user data per vector; vectors of one tiled work item (one tile of
+// one edge) and of one packed work item (consecutive vectors of consecutive
+// edges).  The element-wide variants give a tiled item twice the vectors.
 int variant_in_bytes(Variant v);
 int variant_tile(Variant v);
+int variant_pack_tile(Variant v);
 
 // streaming: nontemporal loads and stores, for operations much larger than
 // the 256 MB Infinity Cache; plain accesses let a small operation's steps
