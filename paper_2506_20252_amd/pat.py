@@ -170,6 +170,63 @@ def pat_reducescatter(sendbufs, recvbufs, count, dtype, op, nranks, stream=None)
                                    int(op), int(nranks), _stream(stream))
 
 
+# ---------------------------------------------------------------------------
+# Tensor-level convenience: the same two calls, with the rank count, count and
+# dtype read from torch tensors.  Marshalling only; the checks below are the
+# shapes the C calls document.  Building the pointer arrays costs O(N) Python
+# per call: a caller in a hot loop builds them once with pointer_array() and
+# calls pat_allgather / pat_reducescatter directly.
+# ---------------------------------------------------------------------------
+
+_TORCH_DTYPES = {"torch.int32": "int32", "torch.float32": "float32", "torch.bfloat16": "bfloat16"}
+
+
+def _rows(t, what):
+    """A 2-D tensor is one row per rank; a list or tuple is taken as is."""
+    if isinstance(t, (list, tuple)):
+        return list(t)
+    if getattr(t, "dim", lambda: 0)() != 2:
+        raise ValueError(f"{what}: a 2-D tensor (one row per rank) or a list of per-rank tensors")
+    return list(t)
+
+
+def _dtype_of(rows, what):
+    names = {str(r.dtype) for r in rows}
+    if len(names) != 1 or next(iter(names)) not in _TORCH_DTYPES:
+        raise ValueError(f"{what}: one dtype of int32, float32 or bfloat16 for every rank, got {sorted(names)}")
+    return _TORCH_DTYPES[next(iter(names))]
+
+
+def allgather(send, recv, stream=None):
+    """recv[r] = concatenation of send[0..N-1] for every rank r.  send: N rows
+    of `count` elements; recv: N rows of N * count elements, same dtype.
+    Raises PatError on a failed call."""
+    s_rows, r_rows = _rows(send, "send"), _rows(recv, "recv")
+    n = len(s_rows)
+    if n < 1 or len(r_rows) != n:
+        raise ValueError("send and recv need one row per rank, as many of each")
+    count = s_rows[0].numel()
+    if any(r.numel() != count for r in s_rows) or any(r.numel() != n * count for r in r_rows):
+        raise ValueError("send rows hold `count` elements, recv rows N * count")
+    dtype = _dtype_of(s_rows + r_rows, "allgather")
+    return check(pat_allgather(s_rows, r_rows, count, dtype, n, stream), "pat_allgather")
+
+
+def reducescatter(send, recv, stream=None):
+    """recv[R] = sum over x of send[x][R * count : (R + 1) * count].  send: N
+    rows of N * count elements; recv: N rows of `count`, same dtype (bf16
+    sums accumulate in float32).  Raises PatError on a failed call."""
+    s_rows, r_rows = _rows(send, "send"), _rows(recv, "recv")
+    n = len(s_rows)
+    if n < 1 or len(r_rows) != n:
+        raise ValueError("send and recv need one row per rank, as many of each")
+    count = r_rows[0].numel()
+    if any(r.numel() != count for r in r_rows) or any(r.numel() != n * count for r in s_rows):
+        raise ValueError("recv rows hold `count` elements, send rows N * count")
+    dtype = _dtype_of(s_rows + r_rows, "reducescatter")
+    return check(pat_reducescatter(s_rows, r_rows, count, dtype, PAT_SUM, n, stream), "pat_reducescatter")
+
+
 def pat_set_buffer_bytes(nbytes):
     return lib().pat_set_buffer_bytes(int(nbytes))
 

@@ -128,3 +128,24 @@ def test_ceiling_probe_library_exports_and_checks_arguments():
         assert fn(*([None] + good[1:]), 4096, None) == invalid, name
         assert fn(*(good[:-1] + [good[-1] + 8]), 4096, None) == invalid, name
         assert fn(*good, 4100, None) == invalid, name
+
+
+def test_tensor_wrappers_check_shapes_and_dtypes_before_any_call():
+    """The tensor-level allgather / reducescatter read N, count and dtype from
+    the tensors and refuse inconsistent ones with ValueError before calling
+    the library (host tensors here: no call may reach a device)."""
+    import torch
+
+    bad = [
+        (pat.allgather, torch.zeros(4, 3), torch.zeros(4, 11)),                 # recv rows not N * count
+        (pat.allgather, torch.zeros(4, 3), torch.zeros(3, 12)),                 # rank counts differ
+        (pat.allgather, torch.zeros(4, 3, dtype=torch.float64), torch.zeros(4, 12, dtype=torch.float64)),
+        (pat.allgather, torch.zeros(4, 3), torch.zeros(4, 12, dtype=torch.bfloat16)),  # mixed dtypes
+        (pat.allgather, torch.zeros(12), torch.zeros(48)),                      # 1-D: rows unknown
+        (pat.reducescatter, torch.zeros(4, 12), torch.zeros(4, 4)),             # send rows not N * count
+        (pat.reducescatter, [torch.zeros(12)] * 4, [torch.zeros(3)] * 3),
+        (pat.reducescatter, torch.zeros(0, 0), torch.zeros(0, 0)),              # no ranks
+    ]
+    for fn, send, recv in bad:
+        with pytest.raises(ValueError):
+            fn(send, recv)

@@ -601,6 +601,27 @@ def test_graph_mode_follows_fusion_changes_on_one_plan():
     assert (np.abs(outs[0].astype(np.float64) - exact) <= 1e-5 * scale).all()
 
 
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+def test_tensor_wrappers(dtype):
+    """pat.allgather / pat.reducescatter on 2-D tensors (one row per rank) and
+    on lists of rows give the oracle's results."""
+    n, count, seed = 9, 1000, 0x7E5
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode("stream"))
+    send = torch.empty((n, count), dtype=TORCH[dtype], device=dev)
+    fill_ranks(send, DIST[dtype], seed)
+    recv = torch.empty((n, n * count), dtype=TORCH[dtype], device=dev)
+    pat.allgather(send, recv)
+    host_in = np.stack([synth.host_buffer(DIST[dtype], seed, x, count) for x in range(n)])
+    np.testing.assert_array_equal(as_bits(recv).reshape(n, n, count), D.allgather(host_in))
+    rs_in = torch.empty((n, n * count), dtype=TORCH[dtype], device=dev)
+    fill_ranks(rs_in, DIST[dtype], seed + 1)
+    out = torch.empty((n, count), dtype=TORCH[dtype], device=dev)
+    pat.reducescatter(list(rs_in), list(out))
+    check_rs(as_bits(out), host_rs_inputs(n, count, DIST[dtype], seed + 1), dtype,
+             oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+
+
 def test_pointer_checks_follow_every_argument():
     """The per-pointer checks are skipped only for the exact pointer set a
     thread last validated with the same operation, rank count, count and
