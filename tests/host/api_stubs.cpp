@@ -1,0 +1,29 @@
+// Host-only stand-ins for the kernel entry points of kernels.hip, so that the
+// C-ABI layer (api.cpp) can be built with g++ under the sanitizers.  Launches
+// do nothing and succeed: no kernel runs, so nothing ever reads the fake
+// buffer addresses the checks use.  The sizes follow kernels.hip's variants;
+// they only shape the launch-level steps the host code builds.
+#include "kernels.hpp"
+
+namespace pat {
+
+int variant_in_bytes(Variant v) {
+  switch (v) {
+    case kAgVec: case kRsI32Vec: case kRsF32Vec: return 16;
+    case kRsB16Vec: return 8;
+    case kAgS4: case kRsI32S: case kRsF32S: return 4;
+    default: return 2;
+  }
+}
+int variant_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 2048 : v == kRsB16Vec ? 1024 : 512; }
+int variant_pack_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 1024 : v == kRsB16Vec ? 1024 : 512; }
+
+hipError_t launch_step(Variant, bool, int64_t, const KCtx&, const DevStep&, hipStream_t) { return hipSuccess; }
+hipError_t launch_tree(Variant, bool, const KCtx&, const TreeRange&, hipStream_t) { return hipSuccess; }
+hipError_t launch_persistent(Variant, bool, const KCtx&, int, hipStream_t) { return hipSuccess; }
+hipError_t persistent_capacity(Variant, bool, int* blocks) {
+  *blocks = 1024;
+  return hipSuccess;
+}
+
+}  // namespace pat
