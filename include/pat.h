@@ -31,8 +31,13 @@
  *     ordered on one stream (or otherwise serialised by the caller).
  *   - Pointers must be aligned to the element size.  When every pointer is
  *     16-byte aligned and count * sizeof(element) is a multiple of 16, the
- *     kernels move 128-bit vectors; otherwise they move single elements
- *     (correct, slower).
+ *     kernels move 128-bit vectors.  Otherwise they still move 128-bit
+ *     vectors, at element-aligned addresses, as long as every piece of a
+ *     chunk holds at least one (16 bytes): a piece's last, partial vector is
+ *     moved back to end where the piece ends and stores only its own
+ *     elements.  bf16 reduce-scatters take this path only for pieces of a
+ *     multiple of 4 elements.  Other pieces move single elements (correct,
+ *     slower).
  *   - In place is allowed only in the MPI/NCCL form given per operation;
  *     any other overlap between a receive buffer and another buffer is
  *     PAT_ERR_INVALID_ARGUMENT.  Send buffers may overlap each other.
@@ -186,7 +191,10 @@ typedef struct {
   int steps;                  /* communication steps per piece */
   int pieces;                 /* pieces a chunk is split into (1 unless chunk > budget) */
   int max_chunks_per_step;    /* largest number of chunks a rank sends in one step */
-  int vector_path;            /* 1: 128-bit kernels possible for aligned pointers */
+  int vector_path;            /* path taken with 16-byte-aligned pointers: 1 aligned 128-bit
+                                 vectors; 2 128-bit vectors with a partial last vector per piece
+                                 (also the path of element-aligned pointers whenever it is not 0);
+                                 0 single elements (a piece under one vector) */
   size_t count;               /* elements per chunk */
   size_t piece_elems;         /* elements per piece */
   size_t slot_elem_bytes;     /* 4 for bf16 reduce-scatter (float32 partials) */
@@ -197,7 +205,7 @@ typedef struct {
   double alg_bytes;           /* memory bytes the steps must read + write per operation */
   double bus_bytes_per_rank;  /* (nranks - 1) * count * sizeof(dtype) */
   int fused_steps;            /* steps run as one fused launch (stream/graph modes, current setting) */
-  int launches_per_op;        /* kernel launches per operation in stream mode (128-bit path if possible) */
+  int launches_per_op;        /* kernel launches per operation in stream mode (path vector_path) */
   int streaming;              /* 1: nontemporal loads and stores (operations of >= 1e9 algorithmic bytes) */
   int xcd_run;                /* step kernels: each XCD takes runs of this many consecutive work items
                                  (0: a contiguous eighth of each step; all-gather 0, reduce-scatter 32) */

@@ -200,10 +200,14 @@ size_t entry_stride(size_t bytes) { return bytes >= 256 ? round_up(bytes, 256) :
 struct Plan {
   pat::PlanDesc desc;
   int device = 0;
-  bool has_vec = false;
-  std::vector<pat::DevStep> steps[2];  // [0] element path, [1] 128-bit path
+  // Launch-level steps per path: [0] element-wide, [1] 128-bit vectors at
+  // 16-byte-aligned addresses, [2] relaxed 128-bit vectors (element-aligned
+  // addresses, a partial last vector per piece).  A path is empty where the
+  // plan's sizes rule it out.
+  bool has_path[3] = {true, false, false};
+  std::vector<pat::DevStep> steps[3];
   pat::DevEntry* d_entries = nullptr;
-  pat::DevStep* d_steps[2] = {nullptr, nullptr};
+  pat::DevStep* d_steps[3] = {nullptr, nullptr, nullptr};
   const void** d_send = nullptr;
   void** d_recv = nullptr;
   char* d_slots = nullptr;
@@ -237,8 +241,7 @@ struct Plan {
     if (upload_done) (void)hipEventDestroy(upload_done);
     if (pinned) (void)hipHostFree(pinned);
     (void)hipFree(d_entries);
-    (void)hipFree(d_steps[0]);
-    (void)hipFree(d_steps[1]);
+    for (auto* p : d_steps) (void)hipFree(p);
     (void)hipFree(d_send);
     (void)hipFree(d_recv);
     (void)hipFree(d_slots);
@@ -284,15 +287,27 @@ void make_room(int device, size_t need) {
 // Launch-level steps for one vector width: every schedule step of every piece.
 // Chunk-pieces of at least `pack_tile` vectors are split into tiled work items
 // of `tile` vectors (the last one ragged), smaller ones packed `pack_tile`
-// vectors per work item.
-bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, std::vector<pat::DevStep>* out) {
+// vectors per work item.  `partial` (relaxed variants): a piece may end in a
+// partial vector, but must hold one whole vector; otherwise every piece must
+// be whole vectors.  False when the sizes rule the width out.
+bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, bool partial,
+                 std::vector<pat::DevStep>* out) {
   out->clear();
+  const int64_t per_vec = in_bytes / d.esize_in;  // elements per vector
+  if (per_vec < 1) return false;
   for (int piece = 0; piece < d.pieces; ++piece) {
     const int64_t e0 = int64_t(piece) * d.piece_elems;
     const int64_t len = std::min<int64_t>(d.piece_elems, d.count - e0);
-    const int64_t bytes = len * d.esize_in;
-    if (bytes % in_bytes) return false;
-    const int64_t V = bytes / in_bytes;
+    int64_t V = 0, back = 0;
+    if (partial) {
+      if (len < per_vec) return false;
+      V = (len + per_vec - 1) / per_vec;
+      back = V * per_vec - len;
+    } else {
+      const int64_t bytes = len * d.esize_in;
+      if (bytes % in_bytes) return false;
+      V = bytes / in_bytes;
+    }
     for (size_t j = 0; j < d.exec.size(); ++j) {
       const auto& st = d.exec[j];
       pat::DevStep ds{};
@@ -300,6 +315,7 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, 
       ds.k = st.k;
       ds.entry0 = st.first;
       ds.first = j == 0 ? 1 : 0;
+      ds.back = (int16_t)back;
       ds.e0 = e0;
       ds.V = V;
       const int64_t edges = int64_t(d.N) * st.k;
@@ -316,14 +332,22 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, 
   return true;
 }
 
-pat::Variant variant_for(int coll, pat_dtype_t dt, bool vec) {
-  if (coll == 0) return vec ? pat::kAgVec : (dt == PAT_BFLOAT16 ? pat::kAgS2 : pat::kAgS4);
-  switch (dt) {
-    case PAT_INT32: return vec ? pat::kRsI32Vec : pat::kRsI32S;
-    case PAT_FLOAT32: return vec ? pat::kRsF32Vec : pat::kRsF32S;
-    default: return vec ? pat::kRsB16Vec : pat::kRsB16S;
-  }
+// Kernel variant of a path (0 element-wide, 1 aligned vectors, 2 relaxed vectors).
+pat::Variant variant_for(int coll, pat_dtype_t dt, int path) {
+  static const pat::Variant ag[3][3] = {{pat::kAgS4, pat::kAgVec, pat::kAgVecU},   // int32
+                                        {pat::kAgS4, pat::kAgVec, pat::kAgVecU},   // float32
+                                        {pat::kAgS2, pat::kAgVec, pat::kAgVecU}};  // bfloat16
+  static const pat::Variant rs[3][3] = {{pat::kRsI32S, pat::kRsI32Vec, pat::kRsI32VecU},
+                                        {pat::kRsF32S, pat::kRsF32Vec, pat::kRsF32VecU},
+                                        {pat::kRsB16S, pat::kRsB16Vec, pat::kRsB16VecU}};
+  const int t = dt == PAT_INT32 ? 0 : dt == PAT_FLOAT32 ? 1 : 2;
+  return coll == 0 ? ag[t][path] : rs[t][path];
 }
+
+// The path a plan's 16-byte-aligned buffers take: aligned vectors when every
+// piece is whole vectors, else relaxed vectors when every piece holds one,
+// else element-wide.
+int aligned_path(const bool (&has)[3]) { return has[1] ? 1 : has[2] ? 2 : 0; }
 
 pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int device,
                          Plan** out) {
@@ -331,12 +355,12 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &p->desc)) return PAT_ERR_INVALID_ARGUMENT;
   pat::PlanDesc& d = p->desc;
   p->device = device;
-  const bool vec_ok = (count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
-  const pat::Variant vs = variant_for(coll, dt, false), vv = variant_for(coll, dt, true);
-  if (!build_steps(d, pat::variant_in_bytes(vs), pat::variant_tile(vs), pat::variant_pack_tile(vs), &p->steps[0]))
-    return PAT_ERR_INTERNAL;
-  p->has_vec = vec_ok && build_steps(d, pat::variant_in_bytes(vv), pat::variant_tile(vv), pat::variant_pack_tile(vv),
-                                     &p->steps[1]);
+  for (int path = 0; path < 3; ++path) {
+    const pat::Variant v = variant_for(coll, dt, path);
+    p->has_path[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
+                                    path == 2 && pat::variant_partial(v), &p->steps[path]);
+  }
+  if (!p->has_path[0]) return PAT_ERR_INTERNAL;
   p->streaming = streaming_for(d.alg_bytes);
   p->xcd_run = xcd_run_for(coll);
   p->alg_bytes = d.alg_bytes;
@@ -345,8 +369,8 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
   if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)entry_stride(size_t(d.piece_elems) * 4);
   p->bytes = size_t(p->slot_rank_stride + p->rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
-             (p->steps[0].size() + p->steps[1].size()) * sizeof(pat::DevStep) + 2 * N * sizeof(void*) +
-             pat::queue_words(std::max(p->steps[0].size(), p->steps[1].size())) * sizeof(unsigned);
+             (p->steps[0].size() + p->steps[1].size() + p->steps[2].size()) * sizeof(pat::DevStep) +
+             2 * N * sizeof(void*) + pat::queue_words(p->steps[0].size()) * sizeof(unsigned);
   make_room(device, p->bytes);
 
   // On an allocation failure, release every other cached plan of this device
@@ -371,13 +395,13 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   };
   pat_status_t s;
   if ((s = alloc((void**)&p->d_entries, d.entries.size() * sizeof(pat::DevEntry))) != PAT_OK) return s;
-  for (int v = 0; v < 2; ++v)
+  for (int v = 0; v < 3; ++v)
     if ((s = alloc((void**)&p->d_steps[v], p->steps[v].size() * sizeof(pat::DevStep))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_send, N * sizeof(void*))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_recv, N * sizeof(void*))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_slots, size_t(p->slot_rank_stride) * N)) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_rootacc, size_t(p->rootacc_stride) * N)) != PAT_OK) return s;
-  p->sync_words = pat::queue_words(std::max(p->steps[0].size(), p->steps[1].size()));
+  p->sync_words = pat::queue_words(p->steps[0].size());  // every path has the same steps
   if ((s = alloc((void**)&p->d_sync, p->sync_words * sizeof(unsigned))) != PAT_OK) return s;
   HIP_TRY(hipMemset(p->d_sync, 0, p->sync_words * sizeof(unsigned)));
   if (const char* e = std::getenv("PAT_POISON_SLOTS")) {
@@ -389,7 +413,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   if (!d.entries.empty())
     HIP_TRY(hipMemcpy(p->d_entries, d.entries.data(), d.entries.size() * sizeof(pat::DevEntry),
                       hipMemcpyHostToDevice));
-  for (int v = 0; v < 2; ++v)
+  for (int v = 0; v < 3; ++v)
     if (!p->steps[v].empty())
       HIP_TRY(hipMemcpy(p->d_steps[v], p->steps[v].data(), p->steps[v].size() * sizeof(pat::DevStep),
                         hipMemcpyHostToDevice));
@@ -400,10 +424,10 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
     if (e[0] == '1') {
       std::fprintf(stderr,
                    "[pat] plan coll=%d N=%d count=%lld dtype=%d L=%d t=%d T=%d steps=%zu pieces=%d "
-                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f vec=%d streaming=%d\n",
+                   "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f paths=%d%d%d streaming=%d\n",
                    coll, N, (long long)count, (int)dt, d.sched.L, d.sched.t, d.sched.T, d.exec.size(),
                    d.pieces, d.max_k, d.slots.entries, (long long)(p->slot_rank_stride * N), d.alg_bytes,
-                   (int)p->has_vec, (int)p->streaming);
+                   (int)p->has_path[0], (int)p->has_path[1], (int)p->has_path[2], (int)p->streaming);
     }
   }
   *out = p.get();
@@ -507,8 +531,9 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, order, device, &plan);
     if (s != PAT_OK) return s;
   }
-  vec = vec && plan->has_vec;
-  const int vi = vec ? 1 : 0;
+  // 16-byte-aligned buffers take the plan's best path; others the relaxed
+  // vectors where the sizes allow, else element-wide kernels.
+  const int vi = vec ? aligned_path(plan->has_path) : plan->has_path[2] ? 2 : 0;
 
   bool own_copy = false;
   if (coll == 0)
@@ -561,7 +586,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   cx.queue = plan->d_sync;
   cx.status = plan->d_sync + 2;
 
-  const pat::Variant var = variant_for(coll, dt, vec);
+  const pat::Variant var = variant_for(coll, dt, vi);
   const auto& steps = plan->steps[vi];
   const int mode = mode_now();
   if (mode == PAT_EXEC_PERSISTENT) {
@@ -727,7 +752,14 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   info.steps = (int)d.exec.size();
   info.pieces = d.pieces;
   info.max_chunks_per_step = d.max_k;
-  info.vector_path = (d.count * d.esize_in) % 16 == 0 && (d.piece_elems * d.esize_in) % 16 == 0;
+  bool has[3] = {true, false, false};
+  for (int path = 1; path < 3; ++path) {
+    const pat::Variant v = variant_for((int)coll, dtype, path);
+    std::vector<pat::DevStep> steps;
+    has[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
+                            path == 2 && pat::variant_partial(v), &steps);
+  }
+  info.vector_path = aligned_path(has);
   info.count = count;
   info.piece_elems = (size_t)d.piece_elems;
   info.slot_elem_bytes = (size_t)d.esize_slot;
@@ -741,8 +773,9 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   info.alg_bytes = d.alg_bytes;
   info.bus_bytes_per_rank = double(nranks - 1) * double(count) * d.esize_in;
   {
-    const pat::Variant var = variant_for((int)coll, dtype, info.vector_path != 0);
-    const int64_t V = int64_t(d.piece_elems) * d.esize_in / pat::variant_in_bytes(var);
+    const pat::Variant var = variant_for((int)coll, dtype, info.vector_path);
+    const int64_t per_vec = pat::variant_in_bytes(var) / d.esize_in;
+    const int64_t V = (int64_t(d.piece_elems) + per_vec - 1) / per_vec;
     int s0, s1;
     int64_t tile;
     std::lock_guard<std::mutex> lock(g_mu);

@@ -27,7 +27,9 @@ struct DevStep {
   int32_t d;               // distance: peer = r + d (all-gather) / child = r + d (reduce-scatter)
   int32_t k;               // entries per rank
   int32_t entry0;          // first entry in the entry table
-  int32_t first;           // 1: first step of a piece (all-gather fuses the own-chunk copy here)
+  int16_t first;           // 1: first step of a piece (all-gather fuses the own-chunk copy here)
+  int16_t back;            // relaxed variants: the piece's last vector is partial, this many
+                           // elements short (it is moved back to end at the piece's end); else 0
   int64_t e0;              // first element of the piece within a chunk
   int64_t V;               // vectors per chunk-piece
   int64_t tiles_per_edge;  // > 0: each work item is one tile of one edge; 0: items pack edges

@@ -83,20 +83,59 @@ constexpr int kSTU = PAT_SCALAR_TILED_UNROLL;  // element-wide kernels: tiled pa
 // through an explicit global (address space 1) pointer instead.
 #define PAT_GLOBAL __attribute__((address_space(1)))
 
-template <typename T, bool NT>
+// Access alignment A: 0 keeps the type's own; A > 0 lets a 16-byte vector
+// sit at any A-byte-aligned address (the relaxed variants, for buffers that
+// are only element-aligned).  Code objects for gfx950 run in unaligned-access
+// mode, where such a vector is still one 128-bit load or store.
+template <typename T, int A>
+struct Access {
+  typedef T type __attribute__((aligned(A)));
+};
+template <typename T>
+struct Access<T, 0> {
+  typedef T type;
+};
+
+template <typename T, bool NT, int A = 0>
 __device__ __forceinline__ T ldg(const char* p) {
-  const PAT_GLOBAL T* q = (const PAT_GLOBAL T*)(p);
+  using AT = typename Access<T, A>::type;
+  const PAT_GLOBAL AT* q = (const PAT_GLOBAL AT*)(p);
   if constexpr (NT) return __builtin_nontemporal_load(q);
   return *q;
 }
 
-template <bool NT, typename T>
+template <bool NT, int A = 0, typename T>
 __device__ __forceinline__ void stg(char* p, const T& v) {
-  PAT_GLOBAL T* q = (PAT_GLOBAL T*)(p);
+  using AT = typename Access<T, A>::type;
+  PAT_GLOBAL AT* q = (PAT_GLOBAL AT*)(p);
   if constexpr (NT)
     __builtin_nontemporal_store(v, q);
   else
     *q = v;
+}
+
+// Word q of a vector, as raw bits.
+__device__ __forceinline__ uint32_t word(v4u x, int q) { return x[q]; }
+__device__ __forceinline__ uint32_t word(v2u x, int q) { return x[q]; }
+__device__ __forceinline__ uint32_t word(v4f x, int q) { return __float_as_uint(x[q]); }
+
+// Stores elements [from, n) of the vector x, taken as n elements of EB bytes
+// each (EB = 2 or 4; 2-byte element 2j is the low half of word j).  Used for
+// a chunk-piece's partial last vector, which is moved back to end at the
+// piece's end: its first `from` elements belong to the vector before it.
+template <bool NT, int EB, typename T>
+__device__ __forceinline__ void stg_from(char* p, T x, int from) {
+  static_assert(EB == 2 || EB == 4, "2- or 4-byte elements");
+  constexpr int W = sizeof(T) / 4;
+  if constexpr (EB == 4) {
+#pragma unroll
+    for (int q = 0; q < W; ++q)
+      if (q >= from) stg<NT>(p + 4 * q, word(x, q));
+  } else {
+#pragma unroll
+    for (int q = 0; q < 2 * W; ++q)
+      if (q >= from) stg<NT>(p + 2 * q, (uint16_t)(word(x, q / 2) >> (16 * (q & 1))));
+  }
 }
 
 __device__ __forceinline__ int wrap_add(int a, int b, int n) {
@@ -181,12 +220,16 @@ __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st
 // ---------------------------------------------------------------------------
 
 // U vectors per lane on the packed and fused paths, TU on the tiled path.
-template <typename Unit, int kU, bool NT, int kTU = kU>
+// kA > 0: the relaxed variant (A-byte-aligned 16-byte vectors; a chunk-piece
+// may end in a partial vector, st.back elements short).
+template <typename Unit, int kU, bool NT, int kTU = kU, int kA = 0>
 struct AgOp {
   static constexpr int U = kU;
   static constexpr int TU = kTU;
   static constexpr int kTile = kThreads * TU;      // vectors of one tiled work item
   static constexpr int kPackTile = kThreads * U;   // vectors of one packed work item
+  static constexpr bool kTail = kA > 0;
+  static_assert(!kTail || sizeof(Unit) == 16, "relaxed all-gather moves 16-byte vectors");
 
   struct Edge {
     const char* src;
@@ -217,11 +260,43 @@ struct AgOp {
     return e;
   }
 
-  __device__ static void put(const Edge& e, int64_t v, const Unit& x) {
-    const int64_t o = v * (int64_t)sizeof(Unit);
-    stg<NT>(e.dst + o, x);
-    if (e.dst2) stg<NT>(e.dst2 + o, x);
-    if (e.dst3) stg<NT>(e.dst3 + o, x);
+  // Byte offset of vector v in the chunk-piece.  A partial last vector is
+  // moved back by st.back elements so that it ends where the piece ends: it
+  // loads the tail of the vector before it too, and stores only its own
+  // elements.
+  __device__ static int64_t off(const KCtx& cx, const DevStep& st, int64_t v) {
+    int64_t o = v * (int64_t)sizeof(Unit);
+    if constexpr (kTail)
+      if (v == st.V - 1) o -= st.back * cx.esize;
+    return o;
+  }
+
+  __device__ static void put(const KCtx& cx, const DevStep& st, const Edge& e, int64_t v, const Unit& x) {
+    const int64_t o = off(cx, st, v);
+    if constexpr (kTail) {
+      if (st.back && v == st.V - 1) {
+        if (cx.esize == 4) {
+          stg_from<NT, 4>(e.dst + o, x, st.back);
+          if (e.dst2) stg_from<NT, 4>(e.dst2 + o, x, st.back);
+          if (e.dst3) stg_from<NT, 4>(e.dst3 + o, x, st.back);
+        } else {
+          stg_from<NT, 2>(e.dst + o, x, st.back);
+          if (e.dst2) stg_from<NT, 2>(e.dst2 + o, x, st.back);
+          if (e.dst3) stg_from<NT, 2>(e.dst3 + o, x, st.back);
+        }
+        return;
+      }
+    }
+    stg<NT, kA>(e.dst + o, x);
+    if (e.dst2) stg<NT, kA>(e.dst2 + o, x);
+    if (e.dst3) stg<NT, kA>(e.dst3 + o, x);
+  }
+
+  // Vectors of the chunk-piece that the straight-line full-tile code may take
+  // (all but a partial last one).
+  __device__ static int64_t whole_vecs(const DevStep& st) {
+    if constexpr (kTail) return st.V - (st.back ? 1 : 0);
+    return st.V;
   }
 
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
@@ -232,33 +307,34 @@ struct AgOp {
       split_tile(item, st, &r, &i, &tile);
       const Edge e = edge(cx, st, r, i);
       const int64_t v0 = tile * kTile + threadIdx.x;
-      if ((tile + 1) * kTile <= st.V) {
+      if ((tile + 1) * kTile <= whole_vecs(st)) {
         // Full tile (uniform): straight-line loads, then one store loop per
         // destination, so no store waits for another store.
 #pragma unroll
-        for (int j = 0; j < TU; ++j) x[j] = ldg<Unit, NT>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
+        for (int j = 0; j < TU; ++j)
+          x[j] = ldg<Unit, NT, kA>(e.src + (v0 + j * kThreads) * (int64_t)sizeof(Unit));
 #pragma unroll
-        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+        for (int j = 0; j < TU; ++j) stg<NT, kA>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         if (e.dst2) {
 #pragma unroll
-          for (int j = 0; j < TU; ++j) stg<NT>(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < TU; ++j) stg<NT, kA>(e.dst2 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         if (e.dst3) {
 #pragma unroll
-          for (int j = 0; j < TU; ++j) stg<NT>(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
+          for (int j = 0; j < TU; ++j) stg<NT, kA>(e.dst3 + (v0 + j * kThreads) * (int64_t)sizeof(Unit), x[j]);
         }
         return;
       }
 #pragma unroll
       for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
-        if (v < st.V) x[j] = ldg<Unit, NT>(e.src + v * (int64_t)sizeof(Unit));
+        if (v < st.V) x[j] = ldg<Unit, NT, kA>(e.src + off(cx, st, v));
       }
       wait_loads();
 #pragma unroll
       for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
-        if (v < st.V) put(e, v, x[j]);
+        if (v < st.V) put(cx, st, e, v, x[j]);
       }
     } else {
       const int64_t units = (int64_t)cx.N * st.k * st.V;
@@ -294,11 +370,11 @@ struct AgOp {
       if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) x[j] = ldg<Unit, NT>(e[j].src + vv[j] * (int64_t)sizeof(Unit));
+      if (vv[j] >= 0) x[j] = ldg<Unit, NT, kA>(e[j].src + off(cx, st, vv[j]));
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) put(e[j], vv[j], x[j]);
+      if (vv[j] >= 0) put(cx, st, e[j], vv[j], x[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
@@ -325,6 +401,8 @@ struct TI32V {
   using in_t = v4u;
   using acc_t = v4u;
   static constexpr int kInElem = 4;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -337,6 +415,8 @@ struct TF32V {
   using in_t = v4f;
   using acc_t = v4f;
   static constexpr int kInElem = 4;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -349,6 +429,8 @@ struct TB16V {
   using in_t = v2u;  // 4 bf16, element 2j in the low half of word j
   using acc_t = v4f;
   static constexpr int kInElem = 2;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = true;
   static constexpr int kUnroll = PAT_B16_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -365,6 +447,8 @@ struct TI32S {
   using in_t = uint32_t;
   using acc_t = uint32_t;
   static constexpr int kInElem = 4;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
@@ -377,6 +461,8 @@ struct TF32S {
   using in_t = float;
   using acc_t = float;
   static constexpr int kInElem = 4;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
@@ -389,12 +475,32 @@ struct TB16S {
   using in_t = uint16_t;
   using acc_t = float;
   static constexpr int kInElem = 2;
+  static constexpr int kAlign = 0;  // natural alignment
+  static constexpr bool kPartial = false;
   static constexpr bool kSeparateRoot = true;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
   __device__ static acc_t widen(in_t x) { return __uint_as_float((uint32_t)x << 16); }
   __device__ static in_t narrow(acc_t x) { return (uint16_t)bf16_rne(x); }
   __device__ static acc_t add(acc_t a, acc_t b) { return a + b; }
+};
+
+// Relaxed variants: the vector traits at element alignment, for buffers that
+// are not 16-byte aligned; int32 and float32 chunk-pieces may also end in a
+// partial vector.  bf16 pieces must be whole vectors of 4 elements: the
+// partial-vector stores grow the bf16 op past what the compiler keeps in
+// registers.
+struct TI32U : TI32V {
+  static constexpr int kAlign = 4;
+  static constexpr bool kPartial = true;
+};
+struct TF32U : TF32V {
+  static constexpr int kAlign = 4;
+  static constexpr bool kPartial = true;
+};
+struct TB16U : TB16V {
+  static constexpr int kAlign = 2;
+  static constexpr bool kPartial = false;
 };
 
 template <class R, bool NT>
@@ -405,6 +511,9 @@ struct RsOp {
   static constexpr int TU = R::kTiledUnroll;   // tiled path
   static constexpr int kTile = kThreads * TU;
   static constexpr int kPackTile = kThreads * U;
+  static constexpr int kA = R::kAlign;
+  static constexpr bool kTail = R::kPartial;  // a chunk-piece may end in a partial vector
+  static_assert(!kTail || sizeof(acc_t) == 16, "relaxed reduce-scatter vectors hold 4 elements");
 
   struct Edge {
     const char* child;
@@ -454,38 +563,62 @@ struct RsOp {
       return x;
   }
 
-  __device__ static void store(const Edge& e, int64_t v, const acc_t& x) {
+  // Byte offset of vector v (of type X, 4 elements) in a chunk-piece of V
+  // vectors: a partial last vector is moved back by `back` elements so that
+  // it ends where the piece ends.  Its loads then cover the tail of the
+  // vector before it (values it does not store), its stores only its own
+  // elements.
+  template <typename X>
+  __device__ static int64_t off(int64_t v, int64_t V, int back) {
+    int64_t o = v * (int64_t)sizeof(X);
+    if constexpr (kTail)
+      if (v == V - 1) o -= back * (int64_t)(sizeof(X) / 4);
+    return o;
+  }
+
+  __device__ static void store(const Edge& e, int64_t v, int64_t V, int back, const acc_t& x) {
+    if constexpr (kTail) {
+      if (back && v == V - 1) {
+        if (e.dst_final)
+          stg_from<NT, sizeof(in_t) / 4>(e.dst + off<in_t>(v, V, back), R::narrow(x), back);
+        else
+          stg_from<NT, 4>(e.dst + off<acc_t>(v, V, back), x, back);
+        return;
+      }
+    }
     if (e.dst_final)
-      stg<NT>(e.dst + v * (int64_t)sizeof(in_t), R::narrow(x));
+      stg<NT, kA>(e.dst + v * (int64_t)sizeof(in_t), R::narrow(x));
     else
-      stg<NT>(e.dst + v * (int64_t)sizeof(acc_t), x);
+      stg<NT, kA>(e.dst + v * (int64_t)sizeof(acc_t), x);
   }
 
   // One tile of one edge whose operand kinds are known: every load is issued
   // before any value is used, so a lane keeps 2U loads in flight (a raw bf16
   // input widened right after its load would wait for each load in turn).
   template <bool OWN_RAW, bool CHILD_RAW>
-  __device__ static void tile(const Edge& e, int64_t tile_idx, int64_t V) {
+  __device__ static void tile(const Edge& e, int64_t tile_idx, int64_t V, int back) {
     vec_t<OWN_RAW> a[TU];
     vec_t<CHILD_RAW> b[TU];
     const int64_t v0 = tile_idx * kTile + threadIdx.x;
-    if ((tile_idx + 1) * kTile <= V) {
+    const int64_t whole = kTail && back ? V - 1 : V;  // vectors the straight-line code may take
+    if ((tile_idx + 1) * kTile <= whole) {
       // Full tile (uniform): straight-line code, no per-lane guards.
 #pragma unroll
       for (int j = 0; j < TU; ++j) {
         const int64_t v = v0 + j * kThreads;
-        a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
-        b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+        a[j] = ldg<vec_t<OWN_RAW>, NT, kA>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
+        b[j] = ldg<vec_t<CHILD_RAW>, NT, kA>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
       }
       acc_t sum[TU];
 #pragma unroll
       for (int j = 0; j < TU; ++j) sum[j] = R::add(to_acc<OWN_RAW>(a[j]), to_acc<CHILD_RAW>(b[j]));
       if (R::kSeparateRoot && e.dst_final) {
 #pragma unroll
-        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
+        for (int j = 0; j < TU; ++j)
+          stg<NT, kA>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(in_t), R::narrow(sum[j]));
       } else {
 #pragma unroll
-        for (int j = 0; j < TU; ++j) stg<NT>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
+        for (int j = 0; j < TU; ++j) stg<NT, kA>(e.dst + (v0 + j * kThreads) * (int64_t)sizeof(acc_t), sum[j]);
       }
       return;
     }
@@ -493,8 +626,8 @@ struct RsOp {
     for (int j = 0; j < TU; ++j) {
       const int64_t v = v0 + j * kThreads;
       if (v < V) {
-        a[j] = ldg<vec_t<OWN_RAW>, NT>(e.own + v * (int64_t)sizeof(vec_t<OWN_RAW>));
-        b[j] = ldg<vec_t<CHILD_RAW>, NT>(e.child + v * (int64_t)sizeof(vec_t<CHILD_RAW>));
+        a[j] = ldg<vec_t<OWN_RAW>, NT, kA>(e.own + off<vec_t<OWN_RAW>>(v, V, back));
+        b[j] = ldg<vec_t<CHILD_RAW>, NT, kA>(e.child + off<vec_t<CHILD_RAW>>(v, V, back));
       }
     }
     acc_t sum[TU];
@@ -504,7 +637,7 @@ struct RsOp {
 #pragma unroll
     for (int j = 0; j < TU; ++j) {
       const int64_t v = v0 + j * kThreads;
-      if (v < V) store(e, v, sum[j]);
+      if (v < V) store(e, v, V, back, sum[j]);
     }
   }
 
@@ -515,17 +648,17 @@ struct RsOp {
       split_tile(item, st, &r, &i, &tile_idx);
       const Edge e = edge(cx, st, r, i);
       if constexpr (kSameVec) {
-        tile<false, false>(e, tile_idx, st.V);
+        tile<false, false>(e, tile_idx, st.V, st.back);
       } else if (e.own_in) {
         if (e.child_in)
-          tile<true, true>(e, tile_idx, st.V);
+          tile<true, true>(e, tile_idx, st.V, st.back);
         else
-          tile<true, false>(e, tile_idx, st.V);
+          tile<true, false>(e, tile_idx, st.V, st.back);
       } else {
         if (e.child_in)
-          tile<false, true>(e, tile_idx, st.V);
+          tile<false, true>(e, tile_idx, st.V, st.back);
         else
-          tile<false, false>(e, tile_idx, st.V);
+          tile<false, false>(e, tile_idx, st.V, st.back);
       }
     } else {
       const int64_t units = (int64_t)cx.N * st.k * st.V;
@@ -566,17 +699,17 @@ struct RsOp {
     for (int j = 0; j < U; ++j) {
       if (vv[j] >= 0) {
         if constexpr (kSameVec) {
-          xa[j] = ldg<acc_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
-          xb[j] = ldg<acc_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+          xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
+          xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
         } else {
           if (e[j].own_in)
-            ra[j] = ldg<in_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(in_t));
+            ra[j] = ldg<in_t, NT, kA>(e[j].own + off<in_t>(vv[j], st.V, st.back));
           else
-            xa[j] = ldg<acc_t, NT>(e[j].own + vv[j] * (int64_t)sizeof(acc_t));
+            xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
           if (e[j].child_in)
-            rb[j] = ldg<in_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(in_t));
+            rb[j] = ldg<in_t, NT, kA>(e[j].child + off<in_t>(vv[j], st.V, st.back));
           else
-            xb[j] = ldg<acc_t, NT>(e[j].child + vv[j] * (int64_t)sizeof(acc_t));
+            xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
         }
       }
     }
@@ -594,7 +727,7 @@ struct RsOp {
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) store(e[j], vv[j], sum[j]);
+      if (vv[j] >= 0) store(e[j], vv[j], st.V, st.back, sum[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
@@ -873,6 +1006,10 @@ hipError_t capacity_t(int* blocks) {
     case kRsI32S: return NT ? CALL((RsOp<TI32S, true>)) : CALL((RsOp<TI32S, false>));                    \
     case kRsF32S: return NT ? CALL((RsOp<TF32S, true>)) : CALL((RsOp<TF32S, false>));                    \
     case kRsB16S: return NT ? CALL((RsOp<TB16S, true>)) : CALL((RsOp<TB16S, false>));                    \
+    case kAgVecU: return NT ? CALL((AgOp<v4u, PAT_UNROLL, true, PAT_UNROLL, 2>)) : CALL((AgOp<v4u, PAT_UNROLL, false, PAT_UNROLL, 2>)); \
+    case kRsI32VecU: return NT ? CALL((RsOp<TI32U, true>)) : CALL((RsOp<TI32U, false>));                \
+    case kRsF32VecU: return NT ? CALL((RsOp<TF32U, true>)) : CALL((RsOp<TF32U, false>));                \
+    case kRsB16VecU: return NT ? CALL((RsOp<TB16U, true>)) : CALL((RsOp<TB16U, false>));                \
     default: return hipErrorInvalidValue;                                   \
   }
 
@@ -882,8 +1019,12 @@ int variant_in_bytes(Variant v) {
   switch (v) {
     case kAgVec:
     case kRsI32Vec:
-    case kRsF32Vec: return 16;
-    case kRsB16Vec: return 8;
+    case kRsF32Vec:
+    case kAgVecU:
+    case kRsI32VecU:
+    case kRsF32VecU: return 16;
+    case kRsB16Vec:
+    case kRsB16VecU: return 8;
     case kAgS4:
     case kRsI32S:
     case kRsF32S: return 4;
@@ -892,6 +1033,8 @@ int variant_in_bytes(Variant v) {
     default: return 0;
   }
 }
+
+bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU; }
 
 int variant_tile(Variant v) {
   switch (v) {
@@ -904,6 +1047,10 @@ int variant_tile(Variant v) {
     case kRsI32S: return RsOp<TI32S, true>::kTile;
     case kRsF32S: return RsOp<TF32S, true>::kTile;
     case kRsB16S: return RsOp<TB16S, true>::kTile;
+    case kAgVecU: return AgOp<v4u, PAT_UNROLL, true, PAT_UNROLL, 2>::kTile;
+    case kRsI32VecU: return RsOp<TI32U, true>::kTile;
+    case kRsF32VecU: return RsOp<TF32U, true>::kTile;
+    case kRsB16VecU: return RsOp<TB16U, true>::kTile;
     default: return 0;
   }
 }
@@ -919,6 +1066,10 @@ int variant_pack_tile(Variant v) {
     case kRsI32S: return RsOp<TI32S, true>::kPackTile;
     case kRsF32S: return RsOp<TF32S, true>::kPackTile;
     case kRsB16S: return RsOp<TB16S, true>::kPackTile;
+    case kAgVecU: return AgOp<v4u, PAT_UNROLL, true, PAT_UNROLL, 2>::kPackTile;
+    case kRsI32VecU: return RsOp<TI32U, true>::kPackTile;
+    case kRsF32VecU: return RsOp<TF32U, true>::kPackTile;
+    case kRsB16VecU: return RsOp<TB16U, true>::kPackTile;
     default: return 0;
   }
 }

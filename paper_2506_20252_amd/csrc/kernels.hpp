@@ -51,6 +51,13 @@ enum Variant : int {
   kRsI32S,
   kRsF32S,
   kRsB16S,
+  // Relaxed vectors: 16-byte vectors (bf16 reduce-scatter inputs: 8-byte) at
+  // element-aligned addresses; a chunk-piece may end in a partial vector
+  // (bf16 reduce-scatter: whole vectors only).
+  kAgVecU,
+  kRsI32VecU,
+  kRsF32VecU,
+  kRsB16VecU,
   kNumVariants
 };
 
@@ -60,6 +67,8 @@ enum Variant : int {
 int variant_in_bytes(Variant v);
 int variant_tile(Variant v);
 int variant_pack_tile(Variant v);
+// A chunk-piece may end in a partial vector (relaxed int32/float32/all-gather variants).
+bool variant_partial(Variant v);
 
 // streaming: nontemporal loads and stores, for operations much larger than
 // the 256 MB Infinity Cache; plain accesses let a small operation's steps

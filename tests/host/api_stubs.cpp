@@ -9,14 +9,15 @@ namespace pat {
 
 int variant_in_bytes(Variant v) {
   switch (v) {
-    case kAgVec: case kRsI32Vec: case kRsF32Vec: return 16;
-    case kRsB16Vec: return 8;
+    case kAgVec: case kRsI32Vec: case kRsF32Vec: case kAgVecU: case kRsI32VecU: case kRsF32VecU: return 16;
+    case kRsB16Vec: case kRsB16VecU: return 8;
     case kAgS4: case kRsI32S: case kRsF32S: return 4;
     default: return 2;
   }
 }
-int variant_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 2048 : v == kRsB16Vec ? 1024 : 512; }
-int variant_pack_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 1024 : v == kRsB16Vec ? 1024 : 512; }
+bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU; }
+int variant_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 2048 : v == kRsB16Vec || v == kRsB16VecU ? 1024 : 512; }
+int variant_pack_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 1024 : v == kRsB16Vec || v == kRsB16VecU ? 1024 : 512; }
 
 hipError_t launch_step(Variant, bool, int64_t, const KCtx&, const DevStep&, hipStream_t) { return hipSuccess; }
 hipError_t launch_tree(Variant, bool, const KCtx&, const TreeRange&, hipStream_t) { return hipSuccess; }

@@ -814,3 +814,72 @@ def test_xcd_run_lengths(grain, monkeypatch):
     finally:
         monkeypatch.delenv("PAT_XCD_GRAIN")
         pat.check(pat.pat_finalize())
+
+
+# ---------------------------------------------------------------------------
+# Relaxed 128-bit kernels: element-aligned buffers, partial last vectors
+# ---------------------------------------------------------------------------
+
+def _rows(flat, n, length, skew):
+    """n rows of `length` elements carved from one flat buffer, starting
+    `skew` elements in: every row is element-aligned, most are not 16-byte
+    aligned."""
+    return [flat[skew + r * length: skew + (r + 1) * length] for r in range(n)]
+
+
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+def test_relaxed_vectors_at_element_offsets(dtype, mode):
+    """Buffers one element past a 16-byte boundary, and counts just under,
+    at and over one vector and one tile (a partial last vector that is the
+    only vector, that closes a tile, that opens one), through the relaxed
+    128-bit kernels, against the oracle.  bf16 reduce-scatters take them for
+    counts of a multiple of 4 elements and the element-wide kernels
+    otherwise; plan_info reports the path 16-byte-aligned buffers take."""
+    es = {"int32": 4, "float32": 4, "bfloat16": 2}[dtype]
+    per = 16 // es  # elements per all-gather vector
+    counts = [per - 1, per, per + 1, 2 * per + 3, 2047, 2049, 4100, 4096 * 2 // es - 1]
+    dev = torch.device("cuda:0")
+    pat.check(pat.pat_set_exec_mode(mode))
+    stream = torch.cuda.current_stream()
+    dist = DIST[dtype]
+    for n in (5, 16):
+        for count in counts:
+            seed = 0xA11 + 31 * count + n
+            log(f"[gpu] relaxed n={n} count={count} dtype={dtype} mode={mode}")
+            # all-gather
+            sflat = torch.empty(n * count + 1, dtype=TORCH[dtype], device=dev)
+            rflat = torch.empty(n * n * count + 1, dtype=TORCH[dtype], device=dev)
+            rflat.view(torch.uint8).fill_(0xA5)
+            sends, recvs = _rows(sflat, n, count, 1), _rows(rflat, n, n * count, 1)
+            for r in range(n):
+                synth.fill(sends[r], dist, seed, r)
+            pat.check(pat.pat_allgather(sends, recvs, count, dtype, n, stream), "ag")
+            pat.check(pat.pat_check_device_status(stream), "status")
+            got = as_bits(torch.stack(recvs)).reshape(n, n, count)
+            host_in = np.stack([synth.host_buffer(dist, seed, x, count) for x in range(n)])
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+            # the element before the skewed rows is untouched
+            assert as_bits(rflat[:1]).view(np.uint8).tolist() == [0xA5] * es
+            st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, count, dtype)
+            pat.check(st)
+            assert info["vector_path"] == (0 if count < per else 1 if count % per == 0 else 2)
+            # reduce-scatter
+            sflat = torch.empty(n * n * count + 1, dtype=TORCH[dtype], device=dev)
+            rflat = torch.empty(n * count + 1, dtype=TORCH[dtype], device=dev)
+            rflat.view(torch.uint8).fill_(0x7F)
+            sends, recvs = _rows(sflat, n, n * count, 1), _rows(rflat, n, count, 1)
+            for r in range(n):
+                synth.fill(sends[r], dist, seed + 1, r)
+            pat.check(pat.pat_reducescatter(sends, recvs, count, dtype, pat.PAT_SUM, n, stream), "rs")
+            pat.check(pat.pat_check_device_status(stream), "status")
+            got = as_bits(torch.stack(recvs))
+            check_rs(got, host_rs_inputs(n, count, dist, seed + 1), dtype,
+                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+            assert as_bits(rflat[:1]).view(np.uint8).tolist() == [0x7F] * es
+            st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, n, count, dtype)
+            pat.check(st)
+            # reduce-scatter vectors hold 4 elements (bf16: 8-byte inputs)
+            want = 1 if count % 4 == 0 else 2 if (count >= 4 and dtype != "bfloat16") else 0
+            assert info["vector_path"] == want
+            del sflat, rflat, sends, recvs
