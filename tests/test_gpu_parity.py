@@ -883,3 +883,62 @@ def test_relaxed_vectors_at_element_offsets(dtype, mode):
             want = 1 if count % 4 == 0 else 2 if (count >= 4 and dtype != "bfloat16") else 0
             assert info["vector_path"] == want
             del sflat, rflat, sends, recvs
+
+
+def _skewed_cases(k=60, seed=2027):
+    """A fixed, seeded draw of skewed-buffer configurations."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(k):
+        n = int(rng.choice([2, 3, 6, 9, 24, 64, 130]))
+        dtype = str(rng.choice(["int32", "float32", "bfloat16"]))
+        count = int(rng.choice([4, 7, 12, 64, 333, 1024, 2051, 4099]))
+        budget = int(rng.choice([0, 100, 1000, 4096]))  # small budgets: pieces, each with its partial vector
+        mode = str(rng.choice(["stream", "graph", "persistent"]))
+        fusion = str(rng.choice(["auto", "on", "off"]))
+        order = str(rng.choice(["far", "close"]))
+        coll = str(rng.choice(["ag", "rs"]))
+        skew = int(rng.integers(1, 8))
+        cases.append((coll, n, count, dtype, budget, mode, fusion, order, skew, int(rng.integers(1, 1 << 30))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _skewed_cases(), ids=lambda c: "-".join(str(x) for x in c[:9]))
+def test_random_skewed_buffers(case):
+    """Seeded random mixes with every buffer 1 to 7 elements past a 16-byte
+    boundary (relaxed or element-wide kernels, pieces with partial last
+    vectors), against the oracle."""
+    coll, n, count, dtype, budget, mode, fusion, order, skew, seed = case
+    dev = torch.device("cuda:0")
+    dist = DIST[dtype]
+    pat.check(pat.pat_set_buffer_bytes(budget))
+    pat.check(pat.pat_set_top_fusion(fusion))
+    pat.check(pat.pat_set_linear_order(order))
+    pat.check(pat.pat_set_exec_mode(mode))
+    stream = torch.cuda.current_stream()
+    log(f"[gpu] skewed {case}")
+    try:
+        slen, rlen = (count, n * count) if coll == "ag" else (n * count, count)
+        sflat = torch.empty(n * slen + skew, dtype=TORCH[dtype], device=dev)
+        rflat = torch.empty(n * rlen + skew, dtype=TORCH[dtype], device=dev)
+        rflat.view(torch.uint8).fill_(0x5A)
+        sends, recvs = _rows(sflat, n, slen, skew), _rows(rflat, n, rlen, skew)
+        for r in range(n):
+            synth.fill(sends[r], dist, seed, r)
+        if coll == "ag":
+            pat.check(pat.pat_allgather(sends, recvs, count, dtype, n, stream), "ag")
+            pat.check(pat.pat_check_device_status(stream), "status")
+            got = as_bits(torch.stack(recvs)).reshape(n, n, count)
+            host_in = np.stack([synth.host_buffer(dist, seed, x, count) for x in range(n)])
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+        else:
+            pat.check(pat.pat_reducescatter(sends, recvs, count, dtype, pat.PAT_SUM, n, stream), "rs")
+            pat.check(pat.pat_check_device_status(stream), "status")
+            check_rs(as_bits(torch.stack(recvs)), host_rs_inputs(n, count, dist, seed), dtype,
+                     oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype), order)
+        assert (as_bits(rflat[:skew]).view(np.uint8) == 0x5A).all()
+        del sflat, rflat, sends, recvs
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+        pat.check(pat.pat_set_top_fusion("auto"))
+        pat.check(pat.pat_set_linear_order("far"))
