@@ -91,16 +91,15 @@ int64_t tree_tile_vecs(int N, int64_t V) {
 }
 
 // PAT_FUSION_AUTO fuses the far end of the fusable steps: those that move at
-// most this many bytes (short, latency-bound steps) and whose edges of one
-// tree, times the vectors of one tile, fit a few load rounds per lane.
-// Larger steps keep a kernel each, which spreads their edges over the whole
-// chip.  The byte limit is 128 MiB for reduce-scatters and 64 MiB for
-// all-gathers, whose steps write each byte to two places: measured on
-// MI355X, 128 MiB makes every reduce-scatter tried 1-3% faster, while the
-// all-gather N=1000 with 256 B chunks loses 1.5% (others gain).
+// most 128 MiB (short, latency-bound steps) and whose edges of one tree,
+// times the vectors of one tile, fit a few load rounds per lane.  Larger
+// steps keep a kernel each, which spreads their edges over the whole chip.
+// Measured on MI355X against 64 MiB: reduce-scatters 1-3% faster; all-gathers
+// of 4 KiB chunks 5-7% faster (N = 64 and 128), N = 1000 with 256 B chunks
+// 0.5% faster, others within 0.4%; 256 MiB gains nothing more.
 // PAT_TREE_FUSE_BYTES / PAT_TREE_FUSE_VECS override.
 int64_t tree_fuse_vecs() { return env_or("PAT_TREE_FUSE_VECS", 2048); }
-int64_t tree_fuse_bytes(int coll) { return env_or("PAT_TREE_FUSE_BYTES", int64_t(coll == 1 ? 128 : 64) << 20); }
+int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(128) << 20); }
 
 // Launch-level steps [*s0, *s1) that run as one fused launch, for a plan whose
 // chunk-pieces hold V vectors; empty when nothing is fused.  The candidates
@@ -120,7 +119,7 @@ void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1
   const bool whole = d.sched.M <= 4;
   int lo = whole || d.coll == 0 ? 0 : ns - t, hi = whole || d.coll == 1 ? ns : t;
   if (fusion == PAT_FUSION_AUTO) {
-    const int64_t cap = tree_fuse_vecs(), cap_bytes = tree_fuse_bytes(d.coll);
+    const int64_t cap = tree_fuse_vecs(), cap_bytes = tree_fuse_bytes();
     // bytes a step moves: about three chunk transfers per edge
     auto narrow = [&](int s) {
       const int64_t k = d.exec[s].k;

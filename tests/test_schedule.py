@@ -254,15 +254,13 @@ def test_top_fusion_setting_roundtrip():
 def test_fused_range_reported_by_plan_info(coll):
     """Which steps run as one fused launch (stream and graph modes).  Both
     plans are fully aggregated, so every step may fuse: N=1000 with 256-byte
-    chunks fuses (AUTO) the narrow far steps -- for the all-gather the 7 with
-    at most 62 chunks per rank (the next moves 3 x 1000 x 125 x 256 B, over
-    its 64 MiB limit), for the reduce-scatter 8 (that step is within its
-    128 MiB) -- or (ON) all 10; N=6 with 4 KiB chunks all 3 steps.  A plan
+    chunks fuses (AUTO) the 8 narrow far steps, with at most 125 chunks per
+    rank (the next moves 3 x 1000 x 250 x 256 B, over the 128 MiB limit),
+    or (ON) all 10; N=6 with 4 KiB chunks all 3 steps.  A plan
     with a wider linear part fuses its top part only, and a top part of one
     step is never fused."""
     try:
-        auto = (7, 4) if coll == pat.PAT_ALLGATHER else (8, 3)
-        for fusion, want in (("auto", auto), ("on", (10, 1)), ("off", (0, 10))):
+        for fusion, want in (("auto", (8, 3)), ("on", (10, 1)), ("off", (0, 10))):
             pat.check(pat.pat_set_top_fusion(fusion))
             st, info = pat.pat_plan_info(coll, 1000, 64, "float32")
             assert st == pat.PAT_OK and info["steps"] == 10 and info["t"] == 9
