@@ -346,11 +346,15 @@ def test_sweep_budgets_and_modes(n, budget, mode):
         pat.check(pat.pat_set_buffer_bytes(0))
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph"])
+@pytest.mark.parametrize("count", [1000, 1001, 1004])  # aligned; partial last vectors; bf16 RS 4-element vectors
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 @pytest.mark.parametrize("n", [1, 6, 9])
-def test_in_place(n, dtype, mode):
-    count = 1000
+def test_in_place(n, dtype, mode, count):
+    """MPI-style in place (all-gather: send is chunk r of recv; reduce-scatter:
+    recv is chunk r of send), where a reduce-scatter root's destination is its
+    own input: with odd counts the rows are element-aligned and the relaxed
+    kernels' partial last vectors store into the buffer they load from."""
     got, host_in = run_ag(n, count, dtype, 77 + n, inplace=True, mode=mode)
     np.testing.assert_array_equal(got, D.allgather(host_in))
     got = run_rs(n, count, dtype, 78 + n, inplace=True, mode=mode)
