@@ -415,3 +415,32 @@ def test_slot_memory_follows_the_data(n, count, dtype, coll):
     assert info["slot_bytes_total"] == (info["slot_bytes_per_rank"] + root) * n
     if n == 65536:
         assert info["slot_bytes_per_rank"] == 32767 * 4
+
+
+@pytest.mark.parametrize("coll", [pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER])
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+def test_vector_path_reported_by_plan_info(coll, dtype):
+    """The kernels a plan takes with 16-byte-aligned buffers, as the header
+    states them: aligned vectors when every piece is whole vectors (16 bytes;
+    bf16 reduce-scatter: 4 elements); else relaxed vectors when every piece
+    holds at least one (16 bytes; bf16 reduce-scatters have no partial
+    vectors); else single elements.  Pieces come from small budgets, so the
+    last piece may be under one vector while the others are not."""
+    es = 2 if dtype == "bfloat16" else 4
+    bf16_rs = coll == pat.PAT_REDUCESCATTER and dtype == "bfloat16"
+    per = 4 if coll == pat.PAT_REDUCESCATTER else 16 // es  # elements per vector
+    try:
+        for budget in (0, 48, 100, 1000):
+            pat.check(pat.pat_set_buffer_bytes(budget))
+            for count in (1, 3, 4, 5, 7, 8, 9, 15, 16, 17, 63, 64, 65, 1000, 1001, 1003, 1004):
+                st, info = pat.pat_plan_info(coll, 5, count, dtype)
+                pat.check(st)
+                pe, k = info["piece_elems"], info["pieces"]
+                lens = [pe] * (k - 1) + [count - (k - 1) * pe]
+                assert all(x > 0 for x in lens)
+                whole = all(x % per == 0 for x in lens)
+                holds_one = all(x >= per for x in lens) and not bf16_rs
+                want = 1 if whole else 2 if holds_one else 0
+                assert info["vector_path"] == want, (budget, count, lens)
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
