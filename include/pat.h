@@ -33,11 +33,10 @@
  *     16-byte aligned and count * sizeof(element) is a multiple of 16, the
  *     kernels move 128-bit vectors.  Otherwise they still move 128-bit
  *     vectors, at element-aligned addresses, as long as every piece of a
- *     chunk holds at least one (16 bytes): a piece's last, partial vector is
- *     moved back to end where the piece ends and stores only its own
- *     elements.  bf16 reduce-scatters take this path only for pieces of a
- *     multiple of 4 elements.  Other pieces move single elements (correct,
- *     slower).
+ *     chunk holds at least one (16 bytes; bf16 reduce-scatter: 4 elements):
+ *     a piece's last, partial vector is moved back to end where the piece
+ *     ends and stores only its own elements.  Pieces under one vector move
+ *     single elements (correct, slower).
  *   - In place is allowed only in the MPI/NCCL form given per operation;
  *     any other overlap between a receive buffer and another buffer is
  *     PAT_ERR_INVALID_ARGUMENT.  Send buffers may overlap each other.

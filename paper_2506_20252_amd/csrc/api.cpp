@@ -287,9 +287,11 @@ void make_room(int device, size_t need) {
 // Chunk-pieces of at least `pack_tile` vectors are split into tiled work items
 // of `tile` vectors (the last one ragged), smaller ones packed `pack_tile`
 // vectors per work item.  `partial` (relaxed variants): a piece may end in a
-// partial vector, but must hold one whole vector; otherwise every piece must
-// be whole vectors.  False when the sizes rule the width out.
-bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, bool partial,
+// partial vector, but must hold one whole vector; the partial vector is the
+// piece's last vector, or, with `items`, each edge's takes one lane of work
+// items appended to the step.  Otherwise every piece must be whole vectors.
+// False when the sizes rule the width out.
+bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, bool partial, bool items,
                  std::vector<pat::DevStep>* out) {
   out->clear();
   const int64_t per_vec = in_bytes / d.esize_in;  // elements per vector
@@ -302,6 +304,7 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, 
       if (len < per_vec) return false;
       V = (len + per_vec - 1) / per_vec;
       back = V * per_vec - len;
+      if (items && back) --V;
     } else {
       const int64_t bytes = len * d.esize_in;
       if (bytes % in_bytes) return false;
@@ -325,6 +328,7 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, 
         ds.tiles_per_edge = 0;
         ds.items = (edges * V + pack_tile - 1) / pack_tile;
       }
+      if (items && back) ds.items += (edges + pat::kThreads - 1) / pat::kThreads;  // partial vectors, one per lane
       out->push_back(ds);
     }
   }
@@ -357,7 +361,8 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   for (int path = 0; path < 3; ++path) {
     const pat::Variant v = variant_for(coll, dt, path);
     p->has_path[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
-                                    path == 2 && pat::variant_partial(v), &p->steps[path]);
+                                    path == 2 && pat::variant_partial(v), pat::variant_partial_items(v),
+                                    &p->steps[path]);
   }
   if (!p->has_path[0]) return PAT_ERR_INTERNAL;
   p->streaming = streaming_for(d.alg_bytes);
@@ -756,7 +761,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
     const pat::Variant v = variant_for((int)coll, dtype, path);
     std::vector<pat::DevStep> steps;
     has[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
-                            path == 2 && pat::variant_partial(v), &steps);
+                            path == 2 && pat::variant_partial(v), pat::variant_partial_items(v), &steps);
   }
   info.vector_path = aligned_path(has);
   info.count = count;
@@ -774,7 +779,8 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   {
     const pat::Variant var = variant_for((int)coll, dtype, info.vector_path);
     const int64_t per_vec = pat::variant_in_bytes(var) / d.esize_in;
-    const int64_t V = (int64_t(d.piece_elems) + per_vec - 1) / per_vec;
+    const int64_t V = pat::variant_partial_items(var) ? int64_t(d.piece_elems) / per_vec  // as build_steps counts
+                                                      : (int64_t(d.piece_elems) + per_vec - 1) / per_vec;
     int s0, s1;
     int64_t tile;
     std::lock_guard<std::mutex> lock(g_mu);

@@ -28,12 +28,15 @@ struct DevStep {
   int32_t k;               // entries per rank
   int32_t entry0;          // first entry in the entry table
   int16_t first;           // 1: first step of a piece (all-gather fuses the own-chunk copy here)
-  int16_t back;            // relaxed variants: the piece's last vector is partial, this many
-                           // elements short (it is moved back to end at the piece's end); else 0
+  int16_t back;            // relaxed variants: the piece ends in a partial vector, made of its
+                           // last 4 or 8 elements, which begin this many elements inside the
+                           // last whole vector; 0: no partial vector
   int64_t e0;              // first element of the piece within a chunk
-  int64_t V;               // vectors per chunk-piece
+  int64_t V;               // vectors per chunk-piece: a partial one counts as vector V - 1, or,
+                           // where the step's last work items take it, not at all
   int64_t tiles_per_edge;  // > 0: each work item is one tile of one edge; 0: items pack edges
-  int64_t items;           // work items (workgroups) of this step
+  int64_t items;           // work items (workgroups) of this step; where they take the partial
+                           // vectors, the last ceil(N * k / 256) give each edge's to a lane
 };
 
 }  // namespace pat

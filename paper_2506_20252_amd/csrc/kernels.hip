@@ -171,6 +171,12 @@ __device__ __forceinline__ void split_flat(int64_t g, const DevStep& st, int* r,
 // for all earlier ones, stores included; one wait up front avoids that.
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Work items of a step that cover whole vectors: with a partial vector per
+// edge (st.back > 0), the step's last items give each edge's one to a lane.
+__device__ __forceinline__ int64_t main_items(const KCtx& cx, const DevStep& st) {
+  return st.back ? st.items - ((int64_t)cx.N * st.k + kThreads - 1) / kThreads : st.items;
+}
+
 // Split a tiled work item into (rank, entry, tile).
 __device__ __forceinline__ void split_tile(int64_t item, const DevStep& st, int* r, int* i, int64_t* tile) {
   const int64_t e = item / st.tiles_per_edge;
@@ -377,8 +383,9 @@ struct AgOp {
       if (vv[j] >= 0) put(cx, st, e[j], vv[j], x[j]);
   }
 
-  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
-  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk
+  // (a partial last vector among them).
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool) {
     tree_step_impl<AgOp>(cx, st, c, t0, TV);
   }
 };
@@ -403,6 +410,7 @@ struct TI32V {
   static constexpr int kInElem = 4;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -417,6 +425,7 @@ struct TF32V {
   static constexpr int kInElem = 4;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -431,6 +440,7 @@ struct TB16V {
   static constexpr int kInElem = 2;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = true;
   static constexpr int kUnroll = PAT_B16_UNROLL;
   static constexpr int kTiledUnroll = kUnroll;
@@ -449,6 +459,7 @@ struct TI32S {
   static constexpr int kInElem = 4;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
@@ -463,6 +474,7 @@ struct TF32S {
   static constexpr int kInElem = 4;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = false;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
@@ -477,6 +489,7 @@ struct TB16S {
   static constexpr int kInElem = 2;
   static constexpr int kAlign = 0;  // natural alignment
   static constexpr bool kPartial = false;
+  static constexpr bool kPartialItems = false;
   static constexpr bool kSeparateRoot = true;
   static constexpr int kUnroll = PAT_SCALAR_UNROLL;
   static constexpr int kTiledUnroll = PAT_SCALAR_TILED_UNROLL;
@@ -486,10 +499,7 @@ struct TB16S {
 };
 
 // Relaxed variants: the vector traits at element alignment, for buffers that
-// are not 16-byte aligned; int32 and float32 chunk-pieces may also end in a
-// partial vector.  bf16 pieces must be whole vectors of 4 elements: the
-// partial-vector stores grow the bf16 op past what the compiler keeps in
-// registers.
+// are not 16-byte aligned and chunk-pieces that end in a partial vector.
 struct TI32U : TI32V {
   static constexpr int kAlign = 4;
   static constexpr bool kPartial = true;
@@ -500,7 +510,8 @@ struct TF32U : TF32V {
 };
 struct TB16U : TB16V {
   static constexpr int kAlign = 2;
-  static constexpr bool kPartial = false;
+  static constexpr bool kPartial = true;
+  static constexpr bool kPartialItems = true;  // partial vectors in work items of their own
 };
 
 template <class R, bool NT>
@@ -512,8 +523,12 @@ struct RsOp {
   static constexpr int kTile = kThreads * TU;
   static constexpr int kPackTile = kThreads * U;
   static constexpr int kA = R::kAlign;
-  static constexpr bool kTail = R::kPartial;  // a chunk-piece may end in a partial vector
-  static_assert(!kTail || sizeof(acc_t) == 16, "relaxed reduce-scatter vectors hold 4 elements");
+  // A chunk-piece may end in a partial vector, which either the vector loops
+  // take (kTail) or work items of its own (kItems; the bf16 op, which the
+  // in-loop form grows past what the compiler keeps in registers).
+  static constexpr bool kTail = R::kPartial && !R::kPartialItems;
+  static constexpr bool kItems = R::kPartial && R::kPartialItems;
+  static_assert(!R::kPartial || sizeof(acc_t) == 16, "relaxed reduce-scatter vectors hold 4 elements");
 
   struct Edge {
     const char* child;
@@ -592,6 +607,34 @@ struct RsOp {
       stg<NT, kA>(e.dst + v * (int64_t)sizeof(acc_t), x);
   }
 
+  // One edge's partial last vector as a work item of its own (kItems): the
+  // piece's last 4 elements, which begin st.back elements inside its last
+  // whole vector (st.V counts whole vectors only); only the elements past
+  // that vector are stored.
+  __device__ static void part(const DevStep& st, const Edge& e) {
+    const int64_t in_off = st.V * (int64_t)sizeof(in_t) - st.back * (int64_t)(sizeof(in_t) / 4);
+    const int64_t acc_off = st.V * (int64_t)sizeof(acc_t) - st.back * (int64_t)(sizeof(acc_t) / 4);
+    acc_t a, b;
+    if constexpr (kSameVec) {
+      a = ldg<acc_t, NT, kA>(e.own + acc_off);
+      b = ldg<acc_t, NT, kA>(e.child + acc_off);
+    } else {
+      if (e.own_in)
+        a = R::widen(ldg<in_t, NT, kA>(e.own + in_off));
+      else
+        a = ldg<acc_t, NT, kA>(e.own + acc_off);
+      if (e.child_in)
+        b = R::widen(ldg<in_t, NT, kA>(e.child + in_off));
+      else
+        b = ldg<acc_t, NT, kA>(e.child + acc_off);
+    }
+    const acc_t sum = R::add(a, b);
+    if (e.dst_final)
+      stg_from<NT, sizeof(in_t) / 4>(e.dst + in_off, R::narrow(sum), st.back);
+    else
+      stg_from<NT, 4>(e.dst + acc_off, sum, st.back);
+  }
+
   // One tile of one edge whose operand kinds are known: every load is issued
   // before any value is used, so a lane keeps 2U loads in flight (a raw bf16
   // input widened right after its load would wait for each load in turn).
@@ -642,6 +685,17 @@ struct RsOp {
   }
 
   __device__ static void run(const KCtx& cx, const DevStep& st, int64_t item) {
+    if constexpr (kItems) {
+      const int64_t main = main_items(cx, st);
+      if (item >= main) {  // one lane per edge: its partial last vector
+        const int64_t g = (item - main) * kThreads + threadIdx.x;
+        if (g < (int64_t)cx.N * st.k) {
+          const int r = (int)(g / st.k);
+          part(st, edge(cx, st, r, (int)(g - (int64_t)r * st.k)));
+        }
+        return;
+      }
+    }
     if (st.tiles_per_edge > 0) {
       int r, i;
       int64_t tile_idx;
@@ -730,9 +784,19 @@ struct RsOp {
       if (vv[j] >= 0) store(e[j], vv[j], st.V, st.back, sum[j]);
   }
 
-  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk.
-  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+  // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk;
+  // with kItems the workgroup of the last tile also takes the edges' partial
+  // vectors.
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool last) {
     tree_step_impl<RsOp>(cx, st, c, t0, TV);
+    if constexpr (kItems) {
+      if (last && st.back) {
+        for (int i = threadIdx.x; i < st.k; i += kTreeThreads) {
+          const DevEntry en = cx.entries[st.entry0 + i];
+          part(st, edge_of(cx, st, wrap_add(c, en.p, cx.N), en));
+        }
+      }
+    }
   }
 };
 
@@ -775,7 +839,7 @@ __global__ __launch_bounds__(kTreeThreads) void tree_kernel(KCtx cx, TreeRange t
   for (int s = tr.s0; s < tr.s1; ++s) {
     const DevStep st = cx.steps[s];
     const int64_t left = st.V - t0;
-    Op::tree_step(cx, st, c, t0, left < tr.tile_vecs ? left : tr.tile_vecs);
+    Op::tree_step(cx, st, c, t0, left < tr.tile_vecs ? left : tr.tile_vecs, tile == tr.tiles - 1);
     if (s + 1 < tr.s1) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
@@ -1034,7 +1098,8 @@ int variant_in_bytes(Variant v) {
   }
 }
 
-bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU; }
+bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU || v == kRsB16VecU; }
+bool variant_partial_items(Variant v) { return v == kRsB16VecU; }
 
 int variant_tile(Variant v) {
   switch (v) {

@@ -52,8 +52,7 @@ enum Variant : int {
   kRsF32S,
   kRsB16S,
   // Relaxed vectors: 16-byte vectors (bf16 reduce-scatter inputs: 8-byte) at
-  // element-aligned addresses; a chunk-piece may end in a partial vector
-  // (bf16 reduce-scatter: whole vectors only).
+  // element-aligned addresses; a chunk-piece may end in a partial vector.
   kAgVecU,
   kRsI32VecU,
   kRsF32VecU,
@@ -67,8 +66,12 @@ enum Variant : int {
 int variant_in_bytes(Variant v);
 int variant_tile(Variant v);
 int variant_pack_tile(Variant v);
-// A chunk-piece may end in a partial vector (relaxed int32/float32/all-gather variants).
+// A chunk-piece may end in a partial vector (the relaxed variants).
 bool variant_partial(Variant v);
+// Its partial vector is not among the V the vector loops take: the step's
+// last work items take every edge's, one per lane (the relaxed bf16
+// reduce-scatter).  Otherwise the vector loops take it as vector V - 1.
+bool variant_partial_items(Variant v);
 
 // streaming: nontemporal loads and stores, for operations much larger than
 // the 256 MB Infinity Cache; plain accesses let a small operation's steps

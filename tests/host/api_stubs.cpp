@@ -15,7 +15,8 @@ int variant_in_bytes(Variant v) {
     default: return 2;
   }
 }
-bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU; }
+bool variant_partial(Variant v) { return v == kAgVecU || v == kRsI32VecU || v == kRsF32VecU || v == kRsB16VecU; }
+bool variant_partial_items(Variant v) { return v == kRsB16VecU; }
 int variant_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 2048 : v == kRsB16Vec || v == kRsB16VecU ? 1024 : 512; }
 int variant_pack_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI32S || v == kRsF32S || v == kRsB16S ? 1024 : v == kRsB16Vec || v == kRsB16VecU ? 1024 : 512; }
 

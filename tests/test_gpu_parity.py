@@ -837,9 +837,8 @@ def test_relaxed_vectors_at_element_offsets(dtype, mode):
     """Buffers one element past a 16-byte boundary, and counts just under,
     at and over one vector and one tile (a partial last vector that is the
     only vector, that closes a tile, that opens one), through the relaxed
-    128-bit kernels, against the oracle.  bf16 reduce-scatters take them for
-    counts of a multiple of 4 elements and the element-wide kernels
-    otherwise; plan_info reports the path 16-byte-aligned buffers take."""
+    128-bit kernels, against the oracle; plan_info reports the path
+    16-byte-aligned buffers take."""
     es = {"int32": 4, "float32": 4, "bfloat16": 2}[dtype]
     per = 16 // es  # elements per all-gather vector
     counts = [per - 1, per, per + 1, 2 * per + 3, 2047, 2049, 4100, 4096 * 2 // es - 1]
@@ -884,7 +883,7 @@ def test_relaxed_vectors_at_element_offsets(dtype, mode):
             st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, n, count, dtype)
             pat.check(st)
             # reduce-scatter vectors hold 4 elements (bf16: 8-byte inputs)
-            want = 1 if count % 4 == 0 else 2 if (count >= 4 and dtype != "bfloat16") else 0
+            want = 1 if count % 4 == 0 else 2 if count >= 4 else 0
             assert info["vector_path"] == want
             del sflat, rflat, sends, recvs
 

@@ -423,11 +423,10 @@ def test_vector_path_reported_by_plan_info(coll, dtype):
     """The kernels a plan takes with 16-byte-aligned buffers, as the header
     states them: aligned vectors when every piece is whole vectors (16 bytes;
     bf16 reduce-scatter: 4 elements); else relaxed vectors when every piece
-    holds at least one (16 bytes; bf16 reduce-scatters have no partial
-    vectors); else single elements.  Pieces come from small budgets, so the
-    last piece may be under one vector while the others are not."""
+    holds at least one; else single elements.  Pieces come from small
+    budgets, so the last piece may be under one vector while the others are
+    not."""
     es = 2 if dtype == "bfloat16" else 4
-    bf16_rs = coll == pat.PAT_REDUCESCATTER and dtype == "bfloat16"
     per = 4 if coll == pat.PAT_REDUCESCATTER else 16 // es  # elements per vector
     try:
         for budget in (0, 48, 100, 1000):
@@ -439,7 +438,7 @@ def test_vector_path_reported_by_plan_info(coll, dtype):
                 lens = [pe] * (k - 1) + [count - (k - 1) * pe]
                 assert all(x > 0 for x in lens)
                 whole = all(x % per == 0 for x in lens)
-                holds_one = all(x >= per for x in lens) and not bf16_rs
+                holds_one = all(x >= per for x in lens)
                 want = 1 if whole else 2 if holds_one else 0
                 assert info["vector_path"] == want, (budget, count, lens)
     finally:
