@@ -13,9 +13,14 @@
 // makes the compiler wait for one access before the next.  Accesses use
 // explicit global pointers; loads and stores are nontemporal for operations
 // far larger than the Infinity Cache, and plain (cached) otherwise, so that a
-// small operation's next step finds the slots just written still in cache.  The data path has no matrix work and no
-// reuse, so there is no LDS staging: a load lands in VGPRs and is stored from
-// there.
+// small operation's next step finds the slots just written still in cache.
+// The data path has no matrix work and no reuse, so there is no LDS staging:
+// a load lands in VGPRs and is stored from there.
+//
+// Variants: aligned vectors (16-byte-aligned buffers, whole vectors), relaxed
+// vectors (element-aligned buffers; a chunk-piece may end in a partial
+// vector, which ends where the piece ends and stores only the elements past
+// the vector before it) and single elements (pieces under one vector).
 //
 // All-gather step (section "The PAT algorithm"): the sender at tree position
 // p copies chunk (r - p) mod N from its send buffer (p = 0) or from the slot
