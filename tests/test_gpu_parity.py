@@ -945,3 +945,54 @@ def test_random_skewed_buffers(case):
         pat.check(pat.pat_set_buffer_bytes(0))
         pat.check(pat.pat_set_top_fusion("auto"))
         pat.check(pat.pat_set_linear_order("far"))
+
+
+@pytest.mark.parametrize("case", [
+    ("rs", 128, 2 * MIB - 1, "bfloat16", "stream"),
+    ("rs", 128, 2 * MIB - 3, "bfloat16", "persistent"),
+    ("rs", 64, 262144 - 1, "float32", "stream"),
+    ("rs", 64, 262144 - 3, "int32", "stream"),
+    ("ag", 128, 262144 - 1, "float32", "stream"),
+    ("ag", 128, 524288 - 3, "bfloat16", "stream"),
+], ids=lambda c: "-".join(str(x) for x in c))
+def test_streaming_relaxed_kernels_full_size(case):
+    """Odd counts at the benchmarked sizes: the relaxed kernels in their
+    streaming (nontemporal) form, which only operations of 1e9 or more
+    algorithmic bytes use, against the oracle on sampled outputs that
+    include every chunk's partial last vector and the elements it overlaps."""
+    coll, n, count, dtype, mode = case
+    seed = 0x0DD0 + count
+    dist = DIST[dtype]
+    edge = np.array([0, 1, 2, 3, 4, 7, 8] + [count - k for k in range(1, 10)])
+    rng = np.random.default_rng(count)
+    if coll == "rs":
+        sample = np.unique(np.concatenate([edge, rng.integers(0, count, 1500)]))
+        got = run_rs(n, count, dtype, seed, mode=mode, sample=sample)
+        torch.cuda.empty_cache()
+        check_rs(got, host_rs_inputs(n, count, dist, seed, sample), dtype,
+                 oracle_t(pat.PAT_REDUCESCATTER, n, count, dtype))
+    else:
+        got, host_in = None, None
+        dev = torch.device("cuda:0")
+        log(f"[gpu] all-gather n={n} count={count} {dtype} seed={seed:#x} (full size, odd)")
+        send = torch.empty((n, count), dtype=TORCH[dtype], device=dev)
+        fill_ranks(send, dist, seed)
+        recv = torch.empty((n, n * count), dtype=TORCH[dtype], device=dev)
+        recv.view(torch.uint8).fill_(0xA5)
+        pat.check(pat.pat_set_exec_mode(mode))
+        stream = torch.cuda.current_stream()
+        pat.check(pat.pat_allgather(list(send), list(recv), count, dtype, n, stream), "ag")
+        pat.check(pat.pat_check_device_status(stream), "status")
+        host_in = np.stack([synth.host_buffer(dist, seed, x, count) for x in range(n)])
+        width = np.uint16 if dtype == "bfloat16" else np.uint32
+        want = host_in.view(width)
+        for r in (0, n - 1):
+            np.testing.assert_array_equal(as_bits(recv[r]).view(width), want.reshape(-1))
+        m = 200000
+        rr, xx = rng.integers(0, n, m), rng.integers(0, n, m)
+        ii = np.concatenate([np.tile(edge, 64), rng.integers(0, count, m - 64 * len(edge))])
+        flat = torch.as_tensor(rr * (n * count) + xx * count + ii, device=dev)
+        np.testing.assert_array_equal(as_bits(recv.view(-1)[flat]).view(width), want[xx, ii])
+        del send, recv, flat
+    pat.check(pat.pat_finalize())
+    torch.cuda.empty_cache()
