@@ -519,18 +519,22 @@ def _max_chunks(n, t):
     return max(len(P) for _, P in opat.schedule(n, t))
 
 
-@pytest.mark.parametrize("span", [2, 4])
-@pytest.mark.parametrize("n", [3, 5, 8, 9, 24, 31, 65, 129, 1000])
-@pytest.mark.parametrize("count", [5, 300, 4100])
+def _span_cases():
+    """(count, n, span) with a distinct aggregation level for the span: N = 3
+    reaches full aggregation on the budget of span 4, so it has no span-4
+    case; N = 1000 keeps to the smaller counts."""
+    return [(count, n, span) for count in (5, 300, 4100) for n in (3, 5, 8, 9, 24, 31, 65, 129, 1000)
+            for span in (2, 4) if (n, span) != (3, 4) and not (n == 1000 and count == 4100)]
+
+
+@pytest.mark.parametrize("count,n,span", _span_cases())
 def test_whole_schedule_fused_up_to_span_4(n, count, span):
     """With sub-trees of span 2 (full aggregation) or 4 every step joins the
     fused launch, the linear part included: one launch per operation, the
     oracle's results, and the same bits as one kernel per step."""
     L = opat.ceil_log2(n)
     t = L - (1 if span == 2 else 2)
-    if t < 0 or (n, span) == (3, 4) or (n == 1000 and count == 4100):
-        # N = 3 reaches full aggregation on the budget of span 4
-        pytest.skip("no such level / keep the case small")
+    assert t >= 0
     seed = 0xF0 + 7 * n + count + span
     ran = 0
     try:
