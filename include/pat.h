@@ -165,8 +165,8 @@ int pat_get_exec_mode(void);
  * better left to one kernel each.  AUTO (the default, or the PAT_TOP_FUSION
  * environment variable: auto | on | off) fuses the far end of the fusable
  * range, the steps that move at most 128 MiB and in which one tree's edges
- * over one tile of its chunk
- * amount to at most 2048 vectors, when there are two or more such steps; ON
+ * over one tile of its chunk amount to at most 2048 vectors, when there are
+ * two or more such steps; ON
  * fuses the whole fusable range whenever it has two or more steps.  Neither
  * fuses a chunk that is split into pieces.  A tile is the smallest power of
  * two from 32 to 256 vectors that keeps the launch within 1024 workgroups.
