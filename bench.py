@@ -211,7 +211,9 @@ def small_size_latency(reps=200):
 def other_workloads(reps=50):
     """Workloads 1-3 timed the same way (HIP events around back-to-back
     operations): microseconds per operation, aggregate bus bandwidth and the
-    fraction of HBM peak that the algorithmic bytes reach."""
+    fraction of HBM peak that the algorithmic bytes reach.  Last, workload 3
+    with one element fewer per chunk: rows that are only element-aligned and
+    chunks that end in a partial vector, the relaxed 128-bit kernels' case."""
     import torch
 
     import synth
@@ -221,8 +223,12 @@ def other_workloads(reps=50):
     stream = torch.cuda.current_stream(dev)
     tdt = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}
     rows = []
-    for wid in (1, 2, 3):
+    for wid, odd in ((1, False), (2, False), (3, False), (3, True)):
         coll, n, count, dtype, dist, seed, desc = WORKLOADS[wid]
+        if odd:
+            count -= 1
+            desc = (f"PAT reduce-scatter (sum), N={n} virtual ranks, fp32 N(0,1), {count}-element output chunk "
+                    "(odd count: element-aligned rows, partial last vectors)")
         if coll == "rs":
             send = torch.empty((n, n * count), dtype=tdt[dtype], device=dev)
             recv = torch.empty((n, count), dtype=tdt[dtype], device=dev)
