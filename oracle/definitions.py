@@ -40,12 +40,6 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
-def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp64 to bf16 once (no intermediate fp32 rounding), via PyTorch."""
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
-    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-
-
 def allgather(inputs: np.ndarray) -> np.ndarray:
     """out[r][x] = in[x] for every receiving rank r (a byte copy: any dtype)."""
     inputs = np.asarray(inputs)

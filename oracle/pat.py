@@ -69,6 +69,12 @@ def peer_of(r: int, d: int, nranks: int) -> int:
     return (r + d) % nranks
 
 
+def rank_at(root: int, q: int, nranks: int) -> int:
+    """The rank at position q of the tree rooted at `root` (the inverse of
+    tree_of): positions count forward from the root."""
+    return (root + q) % nranks
+
+
 # --------------------------------------------------------------------------
 # Trees and steps
 # --------------------------------------------------------------------------
@@ -353,3 +359,69 @@ def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far"):
     stats = {"steps": len(steps), "chunks_per_step": [len(P) for _, P in steps],
              "peak_per_dim": peak}
     return out, stats
+
+
+# --------------------------------------------------------------------------
+# Closed form of the reduce-scatter association (far-first linear order)
+# --------------------------------------------------------------------------
+
+def reversed_tree_sum(values, nranks: int, add):
+    """The sum one root obtains with the far-first schedule, written from the
+    tree itself rather than from the steps (section "Conversion to
+    reduce-scatter operations": the trees are reversed, close dimensions come
+    first, and each received partial is added to the receiver's buffer).
+
+    values[q] is the contribution of tree position q (rank root + q).  The node
+    at position lo that owns span w (its reach) first completes the half-span
+    it keeps, then adds the partial of its child at lo + w/2, which owns the
+    other half -- unless truncation removed that child (lo + w/2 >= N).  Close
+    children therefore arrive first, and the association is
+        S(lo, 1) = v[lo]
+        S(lo, w) = S(lo, w/2)                        if lo + w/2 >= N
+                 = add(S(lo, w/2), S(lo + w/2, w/2)) otherwise,
+    evaluated at S(0, 2^L), L = ceil(log2 N).  It does not depend on how many
+    sub-trees run in parallel (T) or on splitting a chunk into pieces.
+
+    `add` is the receiver's addition: a float32 add (one rounding), a wrapping
+    int32 add, or a symbolic one in the pins."""
+    L = ceil_log2(nranks)
+
+    def S(lo, w):
+        if w == 1:
+            return values[lo]
+        left = S(lo, w // 2)
+        if lo + w // 2 >= nranks:
+            return left
+        return add(left, S(lo + w // 2, w // 2))
+
+    return S(0, 1 << L)
+
+
+def reducescatter_closed_form(inputs: np.ndarray, dtype: str) -> np.ndarray:
+    """Reduce-scatter through reversed_tree_sum, destination by destination.
+
+    inputs: (N, N, m), inputs[x][R] = rank x's contribution to chunk R;
+    returns (N, m) in the input dtype.  Tree position q of root R is rank
+    (R + q) mod N (all-gather data moves from r to r + d, so the reversed
+    partials move from r + d to r).  int32 adds wrap; float32 adds round once
+    each; bfloat16 values are widened exactly, added in float32 and rounded to
+    bfloat16 once at the end."""
+    inputs = np.asarray(inputs)
+    N = inputs.shape[0]
+    out = np.empty((N,) + inputs.shape[2:], dtype=inputs.dtype)
+    if dtype == "int32":
+        add = lambda a, b: (a + b).astype(np.uint32)  # noqa: E731  (wraps)
+    elif dtype in ("float32", "bfloat16"):
+        add = lambda a, b: (a + b).astype(np.float32)  # noqa: E731
+    else:
+        raise ValueError(dtype)
+    for R in range(N):
+        v = [_widen(inputs[rank_at(R, q, N), R], dtype) for q in range(N)]
+        total = reversed_tree_sum(v, N, add)
+        if dtype == "int32":
+            out[R] = np.asarray(total, dtype=np.uint32).view(np.int32)
+        elif dtype == "float32":
+            out[R] = total
+        else:
+            out[R] = f32_to_bf16_bits(np.asarray(total, dtype=np.float32))
+    return out

@@ -173,7 +173,8 @@ def pat_reducescatter(sendbufs, recvbufs, count, dtype, op, nranks, stream=None)
 # ---------------------------------------------------------------------------
 # Tensor-level convenience: the same two calls, with the rank count, count and
 # dtype read from torch tensors.  Marshalling only; the checks below are the
-# shapes the C calls document.  Building the pointer arrays costs O(N) Python
+# shapes and placement the C calls document (device memory, element-contiguous
+# rows).  Building the pointer arrays costs O(N) Python
 # per call: a caller in a hot loop builds them once with pointer_array() and
 # calls pat_allgather / pat_reducescatter directly.
 # ---------------------------------------------------------------------------
@@ -190,6 +191,22 @@ def _rows(t, what):
     return list(t)
 
 
+def _check_rows(rows, what):
+    """Every row must be a contiguous device tensor, all on one GPU: the
+    kernels take each row's address as `numel` consecutive elements.  Returns
+    that device."""
+    devices = set()
+    for r in rows:
+        if not hasattr(r, "is_cuda") or not r.is_cuda:
+            raise ValueError(f"{what}: every row must be a GPU tensor (a host address would reach the kernels)")
+        if not (r.is_contiguous() or (r.dim() == 1 and r.numel() <= 1)):
+            raise ValueError(f"{what}: every row must be contiguous (its elements consecutive in memory)")
+        devices.add(r.device)
+    if len(devices) > 1:
+        raise ValueError(f"{what}: all rows must be on one device, got {sorted(str(d) for d in devices)}")
+    return next(iter(devices))
+
+
 def _dtype_of(rows, what):
     names = {str(r.dtype) for r in rows}
     if len(names) != 1 or next(iter(names)) not in _TORCH_DTYPES:
@@ -197,10 +214,23 @@ def _dtype_of(rows, what):
     return _TORCH_DTYPES[next(iter(names))]
 
 
+def _tensor_call_stream(device, stream):
+    """The stream a tensor-level call runs on: the one given, else torch's
+    current stream of the rows' device (so that the call is ordered after the
+    work that produced its inputs, also inside ``torch.cuda.stream(...)``).
+    The rows must be on the current device: the library plans per current
+    device."""
+    import torch
+    if device != torch.device("cuda", torch.cuda.current_device()):
+        raise ValueError(f"rows are on {device}, but the current device is cuda:{torch.cuda.current_device()}")
+    return stream if stream is not None else torch.cuda.current_stream(device)
+
+
 def allgather(send, recv, stream=None):
     """recv[r] = concatenation of send[0..N-1] for every rank r.  send: N rows
-    of `count` elements; recv: N rows of N * count elements, same dtype.
-    Raises PatError on a failed call."""
+    of `count` elements; recv: N rows of N * count elements, same dtype, all
+    on the current GPU with unit stride.  Runs on `stream`, by default torch's
+    current stream.  Raises ValueError on bad rows, PatError on a failed call."""
     s_rows, r_rows = _rows(send, "send"), _rows(recv, "recv")
     n = len(s_rows)
     if n < 1 or len(r_rows) != n:
@@ -209,13 +239,16 @@ def allgather(send, recv, stream=None):
     if any(r.numel() != count for r in s_rows) or any(r.numel() != n * count for r in r_rows):
         raise ValueError("send rows hold `count` elements, recv rows N * count")
     dtype = _dtype_of(s_rows + r_rows, "allgather")
+    stream = _tensor_call_stream(_check_rows(s_rows + r_rows, "allgather"), stream)
     return check(pat_allgather(s_rows, r_rows, count, dtype, n, stream), "pat_allgather")
 
 
 def reducescatter(send, recv, stream=None):
     """recv[R] = sum over x of send[x][R * count : (R + 1) * count].  send: N
     rows of N * count elements; recv: N rows of `count`, same dtype (bf16
-    sums accumulate in float32).  Raises PatError on a failed call."""
+    sums accumulate in float32), all on the current GPU with unit stride.
+    Runs on `stream`, by default torch's current stream.  Raises ValueError on
+    bad rows, PatError on a failed call."""
     s_rows, r_rows = _rows(send, "send"), _rows(recv, "recv")
     n = len(s_rows)
     if n < 1 or len(r_rows) != n:
@@ -224,6 +257,7 @@ def reducescatter(send, recv, stream=None):
     if any(r.numel() != count for r in r_rows) or any(r.numel() != n * count for r in s_rows):
         raise ValueError("recv rows hold `count` elements, send rows N * count")
     dtype = _dtype_of(s_rows + r_rows, "reducescatter")
+    stream = _tensor_call_stream(_check_rows(s_rows + r_rows, "reducescatter"), stream)
     return check(pat_reducescatter(s_rows, r_rows, count, dtype, PAT_SUM, n, stream), "pat_reducescatter")
 
 

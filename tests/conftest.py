@@ -21,3 +21,13 @@ def read_golden(name):
             key, _, val = line.partition(":")
             out[key.strip()] = val.split()
     return out
+
+
+def pytest_sessionstart(session):
+    """Build the C++ oracle if it is missing or older than its source (g++,
+    about a second; the HIP libraries are built by __graft_entry__.build())."""
+    lib = os.path.join(ROOT, "oracle", "liboracle.so")
+    srcs = [os.path.join(ROOT, "oracle", "rs_oracle.cpp"), os.path.join(ROOT, "synth", "synth_host.hpp")]
+    if not os.path.exists(lib) or any(os.path.getmtime(s) > os.path.getmtime(lib) for s in srcs):
+        from oracle import build as oracle_build
+        oracle_build.build()

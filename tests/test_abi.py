@@ -149,3 +149,48 @@ def test_tensor_wrappers_check_shapes_and_dtypes_before_any_call():
     for fn, send, recv in bad:
         with pytest.raises(ValueError):
             fn(send, recv)
+
+
+class _FakeRow:
+    """Just enough of a tensor for the binding's row checks (no GPU needed)."""
+
+    def __init__(self, cuda=True, contiguous=True, device="cuda:0", dtype="torch.float32", numel=8):
+        import torch
+        self.is_cuda = cuda
+        self._contiguous = contiguous
+        self.device = torch.device(device)
+        self.dtype = dtype
+        self._numel = numel
+
+    def is_contiguous(self):
+        return self._contiguous
+
+    def dim(self):
+        return 1
+
+    def numel(self):
+        return self._numel
+
+    def data_ptr(self):
+        raise AssertionError("a rejected row must never reach the C call")
+
+
+def test_tensor_wrappers_reject_host_tensors():
+    """Host tensors never reach the kernels as addresses: the wrappers raise."""
+    import torch
+    send = torch.zeros((4, 8), dtype=torch.float32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        pat.allgather(send, torch.zeros((4, 32), dtype=torch.float32))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        pat.reducescatter(torch.zeros((4, 32), dtype=torch.float32), send)
+
+
+def test_tensor_wrappers_reject_strided_and_mixed_device_rows():
+    rows = [_FakeRow() for _ in range(3)]
+    assert str(pat._check_rows(rows, "x")) == "cuda:0"
+    with pytest.raises(ValueError, match="contiguous"):
+        pat._check_rows(rows + [_FakeRow(contiguous=False)], "x")
+    with pytest.raises(ValueError, match="one device"):
+        pat._check_rows(rows + [_FakeRow(device="cuda:1")], "x")
+    with pytest.raises(ValueError, match="GPU tensor"):
+        pat._check_rows(rows + [_FakeRow(cuda=False)], "x")

@@ -17,7 +17,6 @@ import math
 import numpy as np
 import pytest
 
-from closed_forms import tree_sum
 from conftest import read_golden
 from oracle import bruck, pat
 from oracle import definitions as D
@@ -205,16 +204,48 @@ def test_aggregation_level_fits_budget():
 # --------------------------------------------------------------------------
 
 def closed_form(inputs, dtype):
-    n = inputs.shape[0]
-    out = []
-    for R in range(n):
-        if dtype == "float32":
-            v = [inputs[(R + q) % n, R].astype(np.float32) for q in range(n)]
-        else:
-            v = [D.bf16_bits_to_f32(inputs[(R + q) % n, R]) for q in range(n)]
-        out.append(tree_sum(v, n))
-    out = np.stack(out)
-    return out if dtype == "float32" else D.f32_to_bf16_bits(out)
+    return pat.reducescatter_closed_form(inputs, dtype)
+
+
+def _symbolic(n, root):
+    """The closed form evaluated on names instead of numbers."""
+    names = [f"x{(root + q) % n}" for q in range(n)]
+    out = pat.reversed_tree_sum(names, n, lambda a, b: f"({a}+{b})")
+    return out[1:-1] if out.startswith("(") and n > 1 else out
+
+
+def test_closed_form_association_matches_hand_derivation():
+    """The reversed-tree association written out by hand from the
+    reduce-scatter section (tests/golden/rs_association.txt), for truncated
+    and full trees and shifted roots."""
+    g = read_golden("rs_association.txt")
+    assert len(g) >= 9
+    for key, (want,) in g.items():
+        n, root = (int(v) for v in key[1:].split("_root"))
+        assert _symbolic(n, root) == want, key
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 6, 7, 13, 64, 100])
+def test_closed_form_int32_is_the_plain_sum(n):
+    """Integer adds associate: the closed form must equal the definition,
+    which catches a dropped, doubled or misplaced term."""
+    x = RNG.integers(-2**31, 2**31, size=(n, n, 5), dtype=np.int64).astype(np.int32)
+    assert (closed_form(x, "int32") == D.reducescatter_sum(x, "int32")).all()
+    f = np.zeros((n, n, 1), dtype=np.int64)
+    for s in range(n):
+        f[s] = 1 << (s % 31)
+    if n <= 31:
+        assert (closed_form(f.astype(np.int32), "int32").astype(np.int64) & 0xFFFFFFFF == (1 << n) - 1).all()
+
+
+@pytest.mark.parametrize("n", [5, 24, 128, 1000])
+def test_closed_form_error_bound(n):
+    """|closed form - exact| <= gamma_L * sum|v| (Higham, section 4.2)."""
+    x = RNG.standard_normal((n, n, 3)).astype(np.float32)
+    got = closed_form(x, "float32").astype(np.float64)
+    L = pat.ceil_log2(n)
+    gamma = L * 2.0 ** -24 / (1 - L * 2.0 ** -24)
+    assert (np.abs(got - D.reducescatter_sum(x, "float32")) <= gamma * D.reducescatter_abs_sum(x, "float32")).all()
 
 
 def bf16_inputs(shape):
@@ -405,6 +436,42 @@ def test_planted_near_first_walk_is_caught(monkeypatch):
         test_pat_n8_aggregation_two()
     x = RNG.standard_normal((8, 8, 64)).astype(np.float32)
     out, _ = pat.reducescatter(x, 0, "float32")
+    assert not (out.view(np.uint32) == closed_form(x, "float32").view(np.uint32)).all()
+
+
+def test_planted_ring_order_association_is_caught(monkeypatch):
+    def ring(values, n, add):  # rank after rank, as a ring would add them
+        acc = values[0]
+        for q in range(1, n):
+            acc = add(acc, values[q])
+        return acc
+    monkeypatch.setattr(pat, "reversed_tree_sum", ring)
+    with pytest.raises(AssertionError):
+        test_closed_form_association_matches_hand_derivation()
+
+
+def test_planted_far_child_first_association_is_caught(monkeypatch):
+    def far_first(values, n, add):  # a node adds its farthest child first
+        L = pat.ceil_log2(n)
+
+        def S(lo, w):
+            acc = values[lo]
+            d = w // 2
+            while d >= 1:
+                if lo + d < n:
+                    acc = add(acc, S(lo + d, d))
+                d //= 2
+            return acc
+        return S(0, 1 << L)
+    monkeypatch.setattr(pat, "reversed_tree_sum", far_first)
+    with pytest.raises(AssertionError):
+        test_closed_form_association_matches_hand_derivation()
+
+
+def test_planted_mirrored_positions_in_closed_form_are_caught(monkeypatch):
+    monkeypatch.setattr(pat, "rank_at", lambda root, q, n: (root - q) % n)
+    x = RNG.standard_normal((7, 7, 64)).astype(np.float32)
+    out, _ = pat.reducescatter(x, 1, "float32")
     assert not (out.view(np.uint32) == closed_form(x, "float32").view(np.uint32)).all()
 
 
