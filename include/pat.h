@@ -61,7 +61,9 @@ typedef enum {
   PAT_ERR_OUT_OF_MEMORY = 3,    /* intermediate buffers could not be allocated */
   PAT_ERR_HIP = 4,              /* a HIP runtime call failed; see pat_last_hip_error() */
   PAT_ERR_TIMEOUT = 5,          /* a persistent kernel's step barrier gave up waiting */
-  PAT_ERR_INTERNAL = 6          /* a plan failed its own consistency checks */
+  PAT_ERR_INTERNAL = 6,         /* a plan failed its own consistency checks */
+  PAT_ERR_TOO_LARGE = 7         /* pat_reducescatter_noalloc: the operation needs more than
+                                   PAT_NOALLOC_SCRATCH_BYTES of tables and intermediate buffers */
 } pat_status_t;
 
 typedef enum {
@@ -120,6 +122,37 @@ pat_status_t pat_allgather(const void* const* sendbufs, void* const* recvbufs, s
  */
 pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbufs, size_t count,
                                pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream);
+
+/*
+ * Reduce-scatter that allocates nothing, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Same operation, arguments, summation order, buffer
+ * budget, linear order and fusion settings as pat_reducescatter, and the same
+ * bits; it always runs as per-step kernels on `stream` (the execution-mode
+ * setting does not apply).
+ *
+ * Instead of the plan cache's device memory, every table, intermediate buffer
+ * and float32 root accumulator lives in a fixed array of
+ * PAT_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  The call makes no hipMalloc / hipFree / host
+ * pinning and creates no event, stream or graph; its host-side schedule
+ * tables are built in ordinary host memory.  When the plan or the pointer
+ * set differs from the previous call's on this GPU, the tables are first
+ * copied into the array with host-to-device copies on `stream`; repeated
+ * calls with the same plan and buffers launch kernels only.
+ *
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it must start at zero): calls that may overlap on one
+ * GPU -- on different streams, or from several host threads without ordering
+ * -- race and give undefined results.  Order them on one stream.
+ *
+ * Errors: as pat_reducescatter, plus PAT_ERR_TOO_LARGE (nothing is launched)
+ * when the plan's slots (slot_bytes_total of pat_plan_info) and tables
+ * exceed the array.
+ */
+#define PAT_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+pat_status_t pat_reducescatter_noalloc(const void* const* sendbufs, void* const* recvbufs, size_t count,
+                                       pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream);
 
 /*
  * Intermediate-buffer budget B, in bytes per slot (section "The PAT

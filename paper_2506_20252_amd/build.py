@@ -20,7 +20,7 @@ HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 
 TARGETS = [
     (os.path.join(PKG, "libpat.so"),
-     [os.path.join(CSRC, f) for f in ("plan.cpp", "api.cpp", "kernels.hip")]),
+     [os.path.join(CSRC, f) for f in ("plan.cpp", "api.cpp", "kernels.hip", "noalloc.hip")]),
     (os.path.join(ROOT, "synth", "libpatsynth.so"), [os.path.join(ROOT, "synth", "synth.hip")]),
     (os.path.join(PKG, "libpatceiling.so"), [os.path.join(CSRC, "ceiling.hip")]),
 ]

@@ -196,15 +196,25 @@ size_t entry_stride(size_t bytes) { return bytes >= 256 ? round_up(bytes, 256) :
     }                                                 \
   } while (0)
 
-struct Plan {
+// The host-side part of a plan: schedule tables per path and the constants
+// derived from them.  Building it allocates only ordinary host memory.
+struct HostPlan {
   pat::PlanDesc desc;
-  int device = 0;
   // Launch-level steps per path: [0] element-wide, [1] 128-bit vectors at
   // 16-byte-aligned addresses, [2] relaxed 128-bit vectors (element-aligned
   // addresses, a partial last vector per piece).  A path is empty where the
   // plan's sizes rule it out.
   bool has_path[3] = {true, false, false};
   std::vector<pat::DevStep> steps[3];
+  bool streaming = true;
+  int64_t xcd_run = 1;     // step kernels: work items per XCD run (0: a contiguous eighth)
+  double alg_bytes = 0.0;  // algorithmic bytes of one operation
+  int64_t slot_chunk_stride = 0, slot_rank_stride = 0, rootacc_stride = 0;
+};
+
+struct Plan {
+  HostPlan h;
+  int device = 0;
   pat::DevEntry* d_entries = nullptr;
   pat::DevStep* d_steps[3] = {nullptr, nullptr, nullptr};
   const void** d_send = nullptr;
@@ -213,7 +223,6 @@ struct Plan {
   char* d_rootacc = nullptr;
   unsigned* d_sync = nullptr;  // persistent-kernel counters: [2] status, work queue from [4]
   size_t sync_words = 0;
-  int64_t slot_chunk_stride = 0, slot_rank_stride = 0, rootacc_stride = 0;
   std::vector<const void*> h_send;
   std::vector<void*> h_recv;
   void** pinned = nullptr;  // 2N pointers staged for upload
@@ -223,9 +232,6 @@ struct Plan {
   // change of the fusion setting selects or captures its own graph.
   std::map<std::tuple<int, int, int, int>, hipGraphExec_t> graphs;
   int capacity[pat::kNumVariants][2] = {};
-  bool streaming = true;
-  int64_t xcd_run = 1;     // step kernels: work items per XCD run (0: a contiguous eighth)
-  double alg_bytes = 0.0;  // algorithmic bytes of one operation
   int cus = 0;
   int64_t clock_khz = 0;
   size_t bytes = 0;          // device memory held (slots, accumulators, tables)
@@ -352,29 +358,38 @@ pat::Variant variant_for(int coll, pat_dtype_t dt, int path) {
 // else element-wide.
 int aligned_path(const bool (&has)[3]) { return has[1] ? 1 : has[2] ? 2 : 0; }
 
+// Schedule tables and slot layout of a plan (host memory only).
+pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order,
+                            HostPlan* h) {
+  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &h->desc)) return PAT_ERR_INVALID_ARGUMENT;
+  const pat::PlanDesc& d = h->desc;
+  for (int path = 0; path < 3; ++path) {
+    const pat::Variant v = variant_for(coll, dt, path);
+    h->has_path[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
+                                    path == 2 && pat::variant_partial(v), pat::variant_partial_items(v),
+                                    &h->steps[path]);
+  }
+  if (!h->has_path[0]) return PAT_ERR_INTERNAL;
+  h->streaming = streaming_for(d.alg_bytes);
+  h->xcd_run = xcd_run_for(coll);
+  h->alg_bytes = d.alg_bytes;
+  h->slot_chunk_stride = (int64_t)entry_stride(size_t(d.piece_elems) * d.esize_slot);
+  h->slot_rank_stride = h->slot_chunk_stride * d.slots.entries;
+  h->rootacc_stride = (coll == 1 && dt == PAT_BFLOAT16) ? (int64_t)entry_stride(size_t(d.piece_elems) * 4) : 0;
+  return PAT_OK;
+}
+
 pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int device,
                          Plan** out) {
   auto p = std::make_unique<Plan>();
-  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &p->desc)) return PAT_ERR_INVALID_ARGUMENT;
-  pat::PlanDesc& d = p->desc;
+  const pat_status_t hs = make_host_plan(coll, N, count, dt, budget, order, &p->h);
+  if (hs != PAT_OK) return hs;
+  const HostPlan& h = p->h;
+  const pat::PlanDesc& d = h.desc;
   p->device = device;
-  for (int path = 0; path < 3; ++path) {
-    const pat::Variant v = variant_for(coll, dt, path);
-    p->has_path[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
-                                    path == 2 && pat::variant_partial(v), pat::variant_partial_items(v),
-                                    &p->steps[path]);
-  }
-  if (!p->has_path[0]) return PAT_ERR_INTERNAL;
-  p->streaming = streaming_for(d.alg_bytes);
-  p->xcd_run = xcd_run_for(coll);
-  p->alg_bytes = d.alg_bytes;
-
-  p->slot_chunk_stride = (int64_t)entry_stride(size_t(d.piece_elems) * d.esize_slot);
-  p->slot_rank_stride = p->slot_chunk_stride * d.slots.entries;
-  if (coll == 1 && dt == PAT_BFLOAT16) p->rootacc_stride = (int64_t)entry_stride(size_t(d.piece_elems) * 4);
-  p->bytes = size_t(p->slot_rank_stride + p->rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
-             (p->steps[0].size() + p->steps[1].size() + p->steps[2].size()) * sizeof(pat::DevStep) +
-             2 * N * sizeof(void*) + pat::queue_words(p->steps[0].size()) * sizeof(unsigned);
+  p->bytes = size_t(h.slot_rank_stride + h.rootacc_stride) * N + d.entries.size() * sizeof(pat::DevEntry) +
+             (h.steps[0].size() + h.steps[1].size() + h.steps[2].size()) * sizeof(pat::DevStep) +
+             2 * N * sizeof(void*) + pat::queue_words(h.steps[0].size()) * sizeof(unsigned);
   make_room(device, p->bytes);
 
   // On an allocation failure, release every other cached plan of this device
@@ -400,26 +415,26 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   pat_status_t s;
   if ((s = alloc((void**)&p->d_entries, d.entries.size() * sizeof(pat::DevEntry))) != PAT_OK) return s;
   for (int v = 0; v < 3; ++v)
-    if ((s = alloc((void**)&p->d_steps[v], p->steps[v].size() * sizeof(pat::DevStep))) != PAT_OK) return s;
+    if ((s = alloc((void**)&p->d_steps[v], h.steps[v].size() * sizeof(pat::DevStep))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_send, N * sizeof(void*))) != PAT_OK) return s;
   if ((s = alloc((void**)&p->d_recv, N * sizeof(void*))) != PAT_OK) return s;
-  if ((s = alloc((void**)&p->d_slots, size_t(p->slot_rank_stride) * N)) != PAT_OK) return s;
-  if ((s = alloc((void**)&p->d_rootacc, size_t(p->rootacc_stride) * N)) != PAT_OK) return s;
-  p->sync_words = pat::queue_words(p->steps[0].size());  // every path has the same steps
+  if ((s = alloc((void**)&p->d_slots, size_t(h.slot_rank_stride) * N)) != PAT_OK) return s;
+  if ((s = alloc((void**)&p->d_rootacc, size_t(h.rootacc_stride) * N)) != PAT_OK) return s;
+  p->sync_words = pat::queue_words(h.steps[0].size());  // every path has the same steps
   if ((s = alloc((void**)&p->d_sync, p->sync_words * sizeof(unsigned))) != PAT_OK) return s;
   HIP_TRY(hipMemset(p->d_sync, 0, p->sync_words * sizeof(unsigned)));
   if (const char* e = std::getenv("PAT_POISON_SLOTS")) {
     if (e[0] == '1') {
-      if (p->d_slots) HIP_TRY(hipMemset(p->d_slots, 0xFF, size_t(p->slot_rank_stride) * N));
-      if (p->d_rootacc) HIP_TRY(hipMemset(p->d_rootacc, 0xFF, size_t(p->rootacc_stride) * N));
+      if (p->d_slots) HIP_TRY(hipMemset(p->d_slots, 0xFF, size_t(h.slot_rank_stride) * N));
+      if (p->d_rootacc) HIP_TRY(hipMemset(p->d_rootacc, 0xFF, size_t(h.rootacc_stride) * N));
     }
   }
   if (!d.entries.empty())
     HIP_TRY(hipMemcpy(p->d_entries, d.entries.data(), d.entries.size() * sizeof(pat::DevEntry),
                       hipMemcpyHostToDevice));
   for (int v = 0; v < 3; ++v)
-    if (!p->steps[v].empty())
-      HIP_TRY(hipMemcpy(p->d_steps[v], p->steps[v].data(), p->steps[v].size() * sizeof(pat::DevStep),
+    if (!h.steps[v].empty())
+      HIP_TRY(hipMemcpy(p->d_steps[v], h.steps[v].data(), h.steps[v].size() * sizeof(pat::DevStep),
                         hipMemcpyHostToDevice));
   HIP_TRY(hipHostMalloc((void**)&p->pinned, 2 * size_t(N) * sizeof(void*), hipHostMallocDefault));
   HIP_TRY(hipEventCreateWithFlags(&p->upload_done, hipEventDisableTiming));
@@ -430,8 +445,8 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
                    "[pat] plan coll=%d N=%d count=%lld dtype=%d L=%d t=%d T=%d steps=%zu pieces=%d "
                    "max_k=%d slot_entries/rank=%d slot_bytes=%lld alg_bytes=%.0f paths=%d%d%d streaming=%d\n",
                    coll, N, (long long)count, (int)dt, d.sched.L, d.sched.t, d.sched.T, d.exec.size(),
-                   d.pieces, d.max_k, d.slots.entries, (long long)(p->slot_rank_stride * N), d.alg_bytes,
-                   (int)p->has_path[0], (int)p->has_path[1], (int)p->has_path[2], (int)p->streaming);
+                   d.pieces, d.max_k, d.slots.entries, (long long)(h.slot_rank_stride * N), d.alg_bytes,
+                   (int)h.has_path[0], (int)h.has_path[1], (int)h.has_path[2], (int)h.streaming);
     }
   }
   *out = p.get();
@@ -482,39 +497,121 @@ struct CheckedPointers {
 };
 thread_local CheckedPointers t_checked;
 
-pat_status_t run(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt, int N,
-                 hipStream_t stream) {
+// Argument checks shared by every entry point.  PAT_OK with *nothing set
+// when count == 0 (no pointer is examined then); *vec tells whether every
+// pointer is 16-byte aligned.
+pat_status_t check_args(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt,
+                        int N, bool* vec, bool* nothing) {
+  *nothing = false;
   if (N < 1 || N > kMaxRanks || send == nullptr || recv == nullptr) return PAT_ERR_INVALID_ARGUMENT;
   if (dt != PAT_INT32 && dt != PAT_FLOAT32 && dt != PAT_BFLOAT16) return PAT_ERR_UNSUPPORTED;
   const size_t es = (size_t)elem_size(dt);
   if (count > (size_t(1) << 40) / es || (unsigned __int128)count * es * N > ((unsigned __int128)1 << 62))
     return PAT_ERR_INVALID_ARGUMENT;
-  if (count == 0) return PAT_OK;
+  if (count == 0) {
+    *nothing = true;
+    return PAT_OK;
+  }
   const size_t chunk = count * es;
   CheckedPointers& ck = t_checked;
   const bool checked = ck.coll == coll && ck.N == N && ck.dt == (int)dt && ck.count == count &&
                        !std::memcmp(ck.send.data(), send, N * sizeof(void*)) &&
                        !std::memcmp(ck.recv.data(), recv, N * sizeof(void*));
-  bool vec = ck.vec;
-  if (!checked) {
-    ck.coll = -1;  // invalid until this set passes
-    vec = true;
-    for (int r = 0; r < N; ++r) {
-      if (!send[r] || !recv[r]) return PAT_ERR_INVALID_ARGUMENT;
-      if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % es) return PAT_ERR_INVALID_ARGUMENT;
-      if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % 16) vec = false;
-    }
-    const size_t send_bytes = coll == 0 ? chunk : chunk * N;
-    const size_t recv_bytes = coll == 0 ? chunk * N : chunk;
-    if (!overlaps_ok(coll, send, recv, N, send_bytes, recv_bytes, chunk)) return PAT_ERR_INVALID_ARGUMENT;
-    ck.send.assign(send, send + N);
-    ck.recv.assign(recv, recv + N);
-    ck.N = N;
-    ck.dt = (int)dt;
-    ck.count = count;
-    ck.vec = vec;
-    ck.coll = coll;
+  if (checked) {
+    *vec = ck.vec;
+    return PAT_OK;
   }
+  ck.coll = -1;  // invalid until this set passes
+  bool v = true;
+  for (int r = 0; r < N; ++r) {
+    if (!send[r] || !recv[r]) return PAT_ERR_INVALID_ARGUMENT;
+    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % es) return PAT_ERR_INVALID_ARGUMENT;
+    if (((uintptr_t)send[r] | (uintptr_t)recv[r]) % 16) v = false;
+  }
+  const size_t send_bytes = coll == 0 ? chunk : chunk * N;
+  const size_t recv_bytes = coll == 0 ? chunk * N : chunk;
+  if (!overlaps_ok(coll, send, recv, N, send_bytes, recv_bytes, chunk)) return PAT_ERR_INVALID_ARGUMENT;
+  ck.send.assign(send, send + N);
+  ck.recv.assign(recv, recv + N);
+  ck.N = N;
+  ck.dt = (int)dt;
+  ck.count = count;
+  ck.vec = v;
+  ck.coll = coll;
+  *vec = v;
+  return PAT_OK;
+}
+
+// The path a call takes: 16-byte-aligned buffers take the plan's best path;
+// others the relaxed vectors where the sizes allow, else element-wide kernels.
+int path_for(const HostPlan& h, bool vec) { return vec ? aligned_path(h.has_path) : h.has_path[2] ? 2 : 0; }
+
+// Whether an all-gather copies each rank's own chunk (not in place).
+bool needs_own_copy(int coll, const void* const* send, void* const* recv, int N, size_t chunk) {
+  if (coll != 0) return false;
+  for (int r = 0; r < N; ++r)
+    if ((const char*)send[r] != (const char*)recv[r] + size_t(r) * chunk) return true;
+  return false;
+}
+
+// Kernel context of a call whose tables and buffers sit at the given device
+// addresses.
+pat::KCtx make_ctx(const HostPlan& h, int vi, const void* const* d_send, void* const* d_recv, char* slots,
+                   char* rootacc, const pat::DevEntry* entries, const pat::DevStep* steps, size_t count, int N,
+                   bool own_copy) {
+  pat::KCtx cx{};
+  cx.send = d_send;
+  cx.recv = d_recv;
+  cx.slots = slots;
+  cx.rootacc = rootacc;
+  cx.entries = entries;
+  cx.steps = steps;
+  cx.count = (int64_t)count;
+  cx.slot_chunk_stride = h.slot_chunk_stride;
+  cx.slot_rank_stride = h.slot_rank_stride;
+  cx.rootacc_stride = h.rootacc_stride;
+  cx.esize = (int64_t)h.desc.esize_in;
+  cx.N = N;
+  cx.nsteps = (int32_t)h.steps[vi].size();
+  cx.own_copy = own_copy ? 1 : 0;
+  return cx;
+}
+
+// The fused range of a call (stream and graph modes).
+pat::TreeRange tree_range(const HostPlan& h, int vi) {
+  pat::TreeRange tr{};
+  const auto& steps = h.steps[vi];
+  fused_range(h.desc, steps.empty() ? 0 : steps[0].V, fusion_now(), &tr.s0, &tr.s1, &tr.tile_vecs);
+  if (tr.s1 > tr.s0) tr.tiles = (steps[0].V + tr.tile_vecs - 1) / tr.tile_vecs;
+  return tr;
+}
+
+// Stream-mode launch sequence: one kernel per step, except that the fused
+// range (steps whose slot entries each serve one tree) runs as one launch.
+hipError_t enqueue_stream(const HostPlan& h, int coll, pat_dtype_t dt, int vi, const pat::KCtx& cx,
+                          const pat::TreeRange& tr, hipStream_t q) {
+  const pat::Variant var = variant_for(coll, dt, vi);
+  const auto& steps = h.steps[vi];
+  const bool fuse = tr.s1 > tr.s0;
+  for (int s = 0; s < (int)steps.size(); ++s) {
+    if (fuse && s == tr.s0) {
+      const hipError_t e = pat::launch_tree(var, h.streaming, cx, tr, q);
+      if (e != hipSuccess) return e;
+      s = tr.s1 - 1;
+      continue;
+    }
+    const hipError_t e = pat::launch_step(var, h.streaming, xcd_grain(h.xcd_run), cx, steps[s], q);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+pat_status_t run(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt, int N,
+                 hipStream_t stream) {
+  bool vec = false, nothing = false;
+  const pat_status_t cs = check_args(coll, send, recv, count, dt, N, &vec, &nothing);
+  if (cs != PAT_OK || nothing) return cs;
+  const size_t chunk = count * (size_t)elem_size(dt);
 
   if (N == 1) {
     if (send[0] != recv[0])
@@ -535,14 +632,9 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, order, device, &plan);
     if (s != PAT_OK) return s;
   }
-  // 16-byte-aligned buffers take the plan's best path; others the relaxed
-  // vectors where the sizes allow, else element-wide kernels.
-  const int vi = vec ? aligned_path(plan->has_path) : plan->has_path[2] ? 2 : 0;
-
-  bool own_copy = false;
-  if (coll == 0)
-    for (int r = 0; r < N && !own_copy; ++r)
-      own_copy = (const char*)send[r] != (const char*)recv[r] + size_t(r) * chunk;
+  const HostPlan& h = plan->h;
+  const int vi = path_for(h, vec);
+  const bool own_copy = needs_own_copy(coll, send, recv, N, chunk);
 
   // Pointer tables: upload only when they changed since the last call.  The
   // remembered set is replaced only once its upload is queued.
@@ -563,22 +655,8 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     plan->h_recv.assign(recv, recv + N);
   }
 
-  const pat::PlanDesc& d = plan->desc;
-  pat::KCtx cx{};
-  cx.send = plan->d_send;
-  cx.recv = plan->d_recv;
-  cx.slots = plan->d_slots;
-  cx.rootacc = plan->d_rootacc;
-  cx.entries = plan->d_entries;
-  cx.steps = plan->d_steps[vi];
-  cx.count = (int64_t)count;
-  cx.slot_chunk_stride = plan->slot_chunk_stride;
-  cx.slot_rank_stride = plan->slot_rank_stride;
-  cx.rootacc_stride = plan->rootacc_stride;
-  cx.esize = (int64_t)es;
-  cx.N = N;
-  cx.nsteps = (int32_t)plan->steps[vi].size();
-  cx.own_copy = own_copy ? 1 : 0;
+  pat::KCtx cx = make_ctx(h, vi, plan->d_send, plan->d_recv, plan->d_slots, plan->d_rootacc, plan->d_entries,
+                          plan->d_steps[vi], count, N, own_copy);
   if (plan->clock_khz == 0) {
     int khz = 0, cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, device));
@@ -591,16 +669,16 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   cx.status = plan->d_sync + 2;
 
   const pat::Variant var = variant_for(coll, dt, vi);
-  const auto& steps = plan->steps[vi];
+  const auto& steps = h.steps[vi];
   const int mode = mode_now();
   if (mode == PAT_EXEC_PERSISTENT) {
-    const bool nt = plan->streaming;
+    const bool nt = h.streaming;
     int& capacity = plan->capacity[var][nt ? 1 : 0];
     if (capacity == 0) HIP_TRY(pat::persistent_capacity(var, nt, &capacity));
     int64_t most = 1;
     for (const auto& st : steps) most = std::max(most, st.items);
     int64_t cap = capacity;
-    const double per_step = plan->alg_bytes / double(std::max<size_t>(1, steps.size()));
+    const double per_step = h.alg_bytes / double(std::max<size_t>(1, steps.size()));
     if (const int per_cu = blocks_per_cu_cap(per_step)) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));  // any size is safe
     if (const char* e = std::getenv("PAT_DEBUG"))
@@ -609,27 +687,9 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
                      capacity, plan->cus, grid, cx.nsteps);
     HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
   } else {
-    // Stream and graph modes: one kernel per step, except that a range of
-    // steps whose slot entries each serve one tree may run as one launch.
-    pat::TreeRange tr{};
-    fused_range(d, steps.empty() ? 0 : steps[0].V, fusion_now(), &tr.s0, &tr.s1, &tr.tile_vecs);
-    const bool fuse = tr.s1 > tr.s0;
-    if (fuse) tr.tiles = (steps[0].V + tr.tile_vecs - 1) / tr.tile_vecs;
-    auto enqueue = [&](hipStream_t q) -> hipError_t {
-      for (int s = 0; s < (int)steps.size(); ++s) {
-        if (fuse && s == tr.s0) {
-          const hipError_t e = pat::launch_tree(var, plan->streaming, cx, tr, q);
-          if (e != hipSuccess) return e;
-          s = tr.s1 - 1;
-          continue;
-        }
-        const hipError_t e = pat::launch_step(var, plan->streaming, xcd_grain(plan->xcd_run), cx, steps[s], q);
-        if (e != hipSuccess) return e;
-      }
-      return hipSuccess;
-    };
+    const pat::TreeRange tr = tree_range(h, vi);
     if (mode == PAT_EXEC_STREAM) {
-      HIP_TRY(enqueue(stream));
+      HIP_TRY(enqueue_stream(h, coll, dt, vi, cx, tr, stream));
     } else {
       hipGraphExec_t& exec = plan->graphs[std::make_tuple(vi, cx.own_copy, tr.s0, tr.s1)];
       if (!exec) {
@@ -637,7 +697,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
         HIP_TRY(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
         hipGraph_t g = nullptr;
         hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
-        if (e == hipSuccess) e = enqueue(cs);
+        if (e == hipSuccess) e = enqueue_stream(h, coll, dt, vi, cx, tr, cs);
         const hipError_t e2 = hipStreamEndCapture(cs, &g);
         if (e == hipSuccess) e = e2;
         if (e == hipSuccess) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);
@@ -655,6 +715,110 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   HIP_TRY(hipEventRecord(plan->done, stream));
   plan->used = true;
   plan->last_use = ++g_tick;
+  return PAT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The entry point that allocates nothing: everything the kernels need beyond
+// the caller's buffers lives in the library's fixed per-device scratch array
+// (noalloc.hip).  Per device, the host remembers which plan's tables and which
+// pointer set the scratch holds, so that repeated calls only launch kernels.
+// ---------------------------------------------------------------------------
+
+struct ScratchState {
+  bool have_plan = false;
+  PlanKey key;
+  HostPlan plan;
+  int vi = -1;                     // path whose step table is in the scratch (-1: none)
+  std::vector<const void*> send;   // pointer set in the scratch's tables
+  std::vector<void*> recv;
+  size_t off_entries = 0, off_steps = 0, off_send = 0, off_recv = 0, off_slots = 0, off_rootacc = 0, end = 0;
+};
+std::map<int, ScratchState> g_scratch;  // by device
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Scratch layout of a plan: a reserved line, the entry table, one path's step
+// table (sized for the longest path), the two pointer tables, the slots and
+// the float32 root accumulators.  Returns the bytes it needs.
+size_t scratch_layout(const HostPlan& h, int N, ScratchState* ss) {
+  size_t o = 256;
+  ss->off_entries = o;
+  o = align256(o + h.desc.entries.size() * sizeof(pat::DevEntry));
+  size_t most = 0;
+  for (const auto& v : h.steps) most = std::max(most, v.size());
+  ss->off_steps = o;
+  o = align256(o + most * sizeof(pat::DevStep));
+  ss->off_send = o;
+  o = align256(o + size_t(N) * sizeof(void*));
+  ss->off_recv = o;
+  o = align256(o + size_t(N) * sizeof(void*));
+  ss->off_slots = o;
+  o = align256(o + size_t(h.slot_rank_stride) * N);
+  ss->off_rootacc = o;
+  o = align256(o + size_t(h.rootacc_stride) * N);
+  ss->end = o;
+  return o;
+}
+
+pat_status_t run_noalloc(int coll, const void* const* send, void* const* recv, size_t count, pat_dtype_t dt,
+                         int N, hipStream_t stream) {
+  bool vec = false, nothing = false;
+  const pat_status_t cs = check_args(coll, send, recv, count, dt, N, &vec, &nothing);
+  if (cs != PAT_OK || nothing) return cs;
+  const size_t chunk = count * (size_t)elem_size(dt);
+  if (N == 1) {
+    if (send[0] != recv[0])
+      HIP_TRY(hipMemcpyAsync(recv[0], send[0], chunk, hipMemcpyDeviceToDevice, stream));
+    return PAT_OK;
+  }
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  char* base = nullptr;
+  HIP_TRY(pat::scratch_base(device, &base));  // this device's array (looked up once per device)
+  ScratchState& ss = g_scratch[device];
+  const PlanKey key(coll, N, (int64_t)count, (int)dt, budget_now(), order_now(), device);
+  if (!ss.have_plan || ss.key != key) {
+    // A new plan: its tables must be uploaded before use.
+    ss.have_plan = false;
+    ss.vi = -1;
+    ss.send.clear();
+    ss.recv.clear();
+    ss.plan = HostPlan();
+    const pat_status_t s = make_host_plan(coll, N, (int64_t)count, dt, std::get<4>(key), std::get<5>(key), &ss.plan);
+    if (s != PAT_OK) return s;
+    if (scratch_layout(ss.plan, N, &ss) > pat::scratch_bytes()) return PAT_ERR_TOO_LARGE;
+    ss.key = key;
+    ss.have_plan = true;
+  }
+  const HostPlan& h = ss.plan;
+  const int vi = path_for(h, vec);
+  if (ss.vi != vi) {
+    ss.vi = -1;
+    const auto& entries = h.desc.entries;
+    if (!entries.empty())
+      HIP_TRY(hipMemcpyAsync(base + ss.off_entries, entries.data(), entries.size() * sizeof(pat::DevEntry),
+                             hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipMemcpyAsync(base + ss.off_steps, h.steps[vi].data(), h.steps[vi].size() * sizeof(pat::DevStep),
+                           hipMemcpyHostToDevice, stream));
+    ss.vi = vi;
+  }
+  const bool same = ss.send.size() == size_t(N) && !std::memcmp(ss.send.data(), send, N * sizeof(void*)) &&
+                    !std::memcmp(ss.recv.data(), recv, N * sizeof(void*));
+  if (!same) {
+    ss.send.assign(send, send + N);
+    ss.recv.assign(recv, recv + N);
+    HIP_TRY(hipMemcpyAsync(base + ss.off_send, ss.send.data(), N * sizeof(void*), hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipMemcpyAsync(base + ss.off_recv, ss.recv.data(), N * sizeof(void*), hipMemcpyHostToDevice, stream));
+  }
+  const pat::KCtx cx = make_ctx(h, vi, (const void* const*)(base + ss.off_send), (void* const*)(base + ss.off_recv),
+                                base + ss.off_slots, base + ss.off_rootacc,
+                                (const pat::DevEntry*)(base + ss.off_entries),
+                                (const pat::DevStep*)(base + ss.off_steps), count, N,
+                                needs_own_copy(coll, send, recv, N, chunk));
+  HIP_TRY(enqueue_stream(h, coll, dt, vi, cx, tree_range(h, vi), stream));
   return PAT_OK;
 }
 
@@ -687,6 +851,12 @@ pat_status_t pat_reducescatter(const void* const* sendbufs, void* const* recvbuf
                                pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream) {
   if (op != PAT_SUM) return PAT_ERR_UNSUPPORTED;
   return run(1, sendbufs, recvbufs, count, dtype, nranks, stream);
+}
+
+pat_status_t pat_reducescatter_noalloc(const void* const* sendbufs, void* const* recvbufs, size_t count,
+                                       pat_dtype_t dtype, pat_op_t op, int nranks, hipStream_t stream) {
+  if (op != PAT_SUM) return PAT_ERR_UNSUPPORTED;
+  return run_noalloc(1, sendbufs, recvbufs, count, dtype, nranks, stream);
 }
 
 pat_status_t pat_set_buffer_bytes(size_t bytes_per_slot) {
@@ -857,6 +1027,7 @@ const char* pat_status_string(pat_status_t status) {
     case PAT_ERR_HIP: return "PAT_ERR_HIP";
     case PAT_ERR_TIMEOUT: return "PAT_ERR_TIMEOUT";
     case PAT_ERR_INTERNAL: return "PAT_ERR_INTERNAL";
+    case PAT_ERR_TOO_LARGE: return "PAT_ERR_TOO_LARGE";
     default: return "PAT_ERR_UNKNOWN";
   }
 }

@@ -95,4 +95,9 @@ hipError_t launch_persistent(Variant v, bool streaming, const KCtx& cx, int grid
 // Workgroups of the persistent kernel that fit on the current device at once.
 hipError_t persistent_capacity(Variant v, bool streaming, int* blocks);
 
+// The no-allocation entry point's fixed scratch array (noalloc.hip): its size,
+// and its device address on `device`, which must be the current device.
+size_t scratch_bytes();
+hipError_t scratch_base(int device, char** base);
+
 }  // namespace pat

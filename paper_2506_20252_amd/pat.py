@@ -23,6 +23,9 @@ PAT_ERR_OUT_OF_MEMORY = 3
 PAT_ERR_HIP = 4
 PAT_ERR_TIMEOUT = 5
 PAT_ERR_INTERNAL = 6
+PAT_ERR_TOO_LARGE = 7
+
+NOALLOC_SCRATCH_BYTES = 256 << 20  # PAT_NOALLOC_SCRATCH_BYTES
 
 PAT_INT32 = 0
 PAT_FLOAT32 = 1
@@ -51,7 +54,7 @@ FUSIONS = {"auto": PAT_FUSION_AUTO, "off": PAT_FUSION_OFF, "on": PAT_FUSION_ON}
 
 # Every function include/pat.h declares.
 EXPORTS = (
-    "pat_allgather", "pat_reducescatter", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
+    "pat_allgather", "pat_reducescatter", "pat_reducescatter_noalloc", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
     "pat_set_top_fusion", "pat_get_top_fusion",
     "pat_set_barrier_timeout_us", "pat_plan_info",
@@ -98,6 +101,8 @@ def lib():
             "pat_allgather": ([_P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _P], ctypes.c_int),
             "pat_reducescatter": ([_P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P],
                                   ctypes.c_int),
+            "pat_reducescatter_noalloc": ([_P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int, _P],
+                                          ctypes.c_int),
             "pat_set_buffer_bytes": ([ctypes.c_size_t], ctypes.c_int),
             "pat_get_buffer_bytes": ([], ctypes.c_size_t),
             "pat_set_exec_mode": ([ctypes.c_int], ctypes.c_int),
@@ -168,6 +173,11 @@ def pat_allgather(sendbufs, recvbufs, count, dtype, nranks, stream=None):
 def pat_reducescatter(sendbufs, recvbufs, count, dtype, op, nranks, stream=None):
     return lib().pat_reducescatter(_ptr_array(sendbufs), _ptr_array(recvbufs), int(count), _dtype(dtype),
                                    int(op), int(nranks), _stream(stream))
+
+
+def pat_reducescatter_noalloc(sendbufs, recvbufs, count, dtype, op, nranks, stream=None):
+    return lib().pat_reducescatter_noalloc(_ptr_array(sendbufs), _ptr_array(recvbufs), int(count), _dtype(dtype),
+                                           int(op), int(nranks), _stream(stream))
 
 
 # ---------------------------------------------------------------------------

@@ -90,6 +90,18 @@ int main() {
   EXPECT(pat_reducescatter(rs_send.data(), rs_recv.data(), count, PAT_BFLOAT16, PAT_SUM, n, nullptr) == rs);
   EXPECT(pat_reducescatter(rs_send.data(), rs_recv.data(), 0x10000, PAT_BFLOAT16, PAT_SUM, n, nullptr) ==
          PAT_ERR_INVALID_ARGUMENT);
+  // the entry point that allocates nothing: the same checks; a valid set
+  // stops at the device layer (here: PAT_ERR_HIP), never at the checks
+  const pat_status_t na =
+      pat_reducescatter_noalloc(rs_send.data(), rs_recv.data(), count, PAT_BFLOAT16, PAT_SUM, n, nullptr);
+  EXPECT(na != PAT_ERR_INVALID_ARGUMENT && na != PAT_OK);
+  EXPECT(pat_reducescatter_noalloc(rs_send.data(), rs_recv.data(), 0x10000, PAT_BFLOAT16, PAT_SUM, n, nullptr) ==
+         PAT_ERR_INVALID_ARGUMENT);
+  EXPECT(pat_reducescatter_noalloc(nul.data(), recv.data(), count, PAT_FLOAT32, PAT_SUM, n, nullptr) ==
+         PAT_ERR_INVALID_ARGUMENT);
+  EXPECT(pat_reducescatter_noalloc(rs_send.data(), rs_recv.data(), count, PAT_FLOAT32, (pat_op_t)3, n, nullptr) ==
+         PAT_ERR_UNSUPPORTED);
+  EXPECT(pat_reducescatter_noalloc(rs_send.data(), rs_recv.data(), 0, PAT_FLOAT32, PAT_SUM, n, nullptr) == PAT_OK);
   EXPECT(pat_allgather(nullptr, recv.data(), count, PAT_FLOAT32, n, nullptr) == PAT_ERR_INVALID_ARGUMENT);
   EXPECT(pat_allgather(send.data(), recv.data(), count, PAT_FLOAT32, 0, nullptr) == PAT_ERR_INVALID_ARGUMENT);
   pat_finalize();

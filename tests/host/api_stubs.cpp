@@ -27,5 +27,9 @@ hipError_t persistent_capacity(Variant, bool, int* blocks) {
   *blocks = 1024;
   return hipSuccess;
 }
+// The no-allocation entry point's array does not exist in a host build: its
+// lookup fails, so a valid call stops with PAT_ERR_HIP before any copy.
+size_t scratch_bytes() { return size_t(256) << 20; }
+hipError_t scratch_base(int, char**) { return hipErrorNotSupported; }
 
 }  // namespace pat
