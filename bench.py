@@ -8,13 +8,18 @@ resident in HBM.  One "step" = one whole reduce-scatter over all 128 ranks.
 Prints one JSON line:
 * value      -- aggregate bus bandwidth, N * (N-1) * C / t  (nccl-tests busBW
                 summed over the N virtual ranks; the per-rank figure is
-                bus_gbps_per_rank)
-* roofline   -- algorithmic memory bytes of the dominant kernel per launch /
-                its average launch duration (HIP events on its stream), against
-                the 8 TB/s HBM3E peak; traffic from the committed rocprofv3
-                counter summary when it matches the current kernel source
-* cpu_baseline -- the CPU oracle (numpy, executing the PAT steps) timed on
-                a bounded sample of the same workload, in the same unit
+                bus_gbps_per_rank); t = the mean of the timed operations, each
+                bracketed by its own HIP events (the median is reported too)
+* roofline   -- the dominant kernel's own rate: the algorithmic bytes of its
+                launches / their durations, from a HIP event pair recorded on
+                the kernels' stream around every launch of a traced pass after
+                the timed region; against the 8 TB/s HBM3E peak; traffic from
+                the committed rocprofv3 counter summary when it matches the
+                current kernel source
+* cpu_baseline -- the CPU oracle timed in the same process: for reduce-scatter
+                the threaded C++ oracle (PAT association and fp64 plain sum)
+                over the whole operation on every host CPU, inputs regenerated
+                from the seed; in the same unit
 
 python bench.py [--steps K] [--warmup W] [--mode persistent|graph|stream]
                 [--workload 1..7] [--cpu-seconds S] [--no-cpu-baseline]
@@ -27,6 +32,7 @@ import math
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -114,27 +120,57 @@ def committed_traffic(workload_id, mode):
     return float(m_bytes.group(1))
 
 
-def cpu_baseline(wid, target_seconds, sample_inputs, m_cap):
-    """Time the oracle on a bounded sample: every destination chunk, the first
-    m element positions of each, m calibrated so the run takes ~target.
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((line.split(":", 1)[1].strip() for line in f if line.startswith("model name")), "")
+    except OSError:
+        return ""
 
-    sample_inputs(m) returns the workload's inputs at those positions."""
+
+def cpu_baseline_rs(wid):
+    """The threaded C++ oracle over the whole reduce-scatter: every destination
+    chunk and every element, the PAT association (float32, or int32) and the
+    fp64 plain sum, inputs regenerated from the seed, on every CPU this process
+    may use.  Streams over blocks of destination chunks, so that nothing the
+    size of the send buffers sits in host memory."""
     import numpy as np  # noqa: F401
 
-    from oracle import pat as opat
+    from oracle import native
+
+    coll, n, count, dtype, dist, seed, _ = WORKLOADS[wid]
+    esize = 2 if dtype == "bfloat16" else 4
+    block = max(1, (1 << 24) // count)
+    native.reducescatter(dtype, n, 1, dist=dist, seed=seed)  # load the library and the table first
+    t0 = time.perf_counter()
+    used = 0
+    for r0 in range(0, n, block):
+        out = native.reducescatter(dtype, n, count, dist=dist, seed=seed, r0=r0, r1=min(n, r0 + block),
+                                   want=("pat", "sum"))
+        used = max(used, out["threads"])
+    elapsed = time.perf_counter() - t0
+    bus_bytes = float(n) * (n - 1) * count * esize
+    return {"value": round(bus_bytes / elapsed / 1e9, 3), "unit": "GB/s", "cores": used, "kind": "oracle",
+            "cpu_model": _cpu_model(), "host_cpus_visible": os.cpu_count(),
+            "input_gbps": round(float(n) * n * count * esize / elapsed / 1e9, 3),
+            "sample": f"whole operation: all {n} destination chunks x all {count} elements, N = {n} inputs each "
+                      f"regenerated from the seed; PAT association ({'int32' if dtype == 'int32' else 'float32'}) "
+                      f"and fp64 plain sum; C++ std::thread oracle on {used} threads; {elapsed:.1f} s",
+            "seconds": round(elapsed, 2)}
+
+
+def cpu_baseline_ag(wid, target_seconds, sample_inputs, m_cap):
+    """All-gather: the oracle's definition (concatenation, numpy, one thread)
+    on a bounded sample: every (receiver, chunk) pair, the first m elements of
+    each chunk, m calibrated so the run takes about `target_seconds`."""
+    from oracle import definitions as D
 
     coll, n, count, dtype, dist, seed, _ = WORKLOADS[wid]
     esize = 2 if dtype == "bfloat16" else 4
 
     def run(x):
-        if coll == "rs":
-            t = opat.aggregation_level(n, count * 4, 8 << 20)
-            t0 = time.perf_counter()
-            opat.reducescatter(x, t, dtype)
-        else:
-            t = opat.aggregation_level(n, count * esize, 8 << 20)
-            t0 = time.perf_counter()
-            opat.allgather(x, t)
+        t0 = time.perf_counter()
+        D.allgather(x)
         return time.perf_counter() - t0
 
     m = min(count, m_cap, 2048)
@@ -143,16 +179,10 @@ def cpu_baseline(wid, target_seconds, sample_inputs, m_cap):
         m = int(min(count, m_cap, max(2 * m, m * target_seconds / max(elapsed, 1e-3))))
         elapsed = run(sample_inputs(m))
     bus_bytes = float(n) * (n - 1) * m * esize
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((line.split(":", 1)[1].strip() for line in f if line.startswith("model name")), "")
-    except OSError:
-        pass
-    return {"value": bus_bytes / elapsed / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "cpu_model": model, "host_cpus_visible": os.cpu_count(),
-            "sample": f"all {n} destination chunks x the first {m} of {count} element positions "
-                      f"({m / count:.3g} of the operation); numpy, one thread; {elapsed:.1f} s",
+    return {"value": round(bus_bytes / elapsed / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "cpu_model": _cpu_model(), "host_cpus_visible": os.cpu_count(),
+            "sample": f"all {n} x {n} (receiver, chunk) pairs x the first {m} of {count} elements "
+                      f"({m / count:.3g} of the operation); numpy definition, one thread; {elapsed:.1f} s",
             "seconds": round(elapsed, 2)}
 
 
@@ -191,16 +221,11 @@ def small_size_latency(reps=200):
             code = pat.PAT_ALLGATHER
         for _ in range(5):
             pat.check(op())
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(reps):
-            pat.check(op())
-        e1.record(stream)
-        torch.cuda.synchronize()
+        mean_ms, per = time_pair_and_reps(op, stream, reps)
         pat.check(pat.pat_check_device_status(stream))
         st, info = pat.pat_plan_info(code, n, count, "float32")
-        out[f"{coll}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+        out[f"{coll}_us"] = round(mean_ms * 1e3, 2)
+        out[f"{coll}_median_us"] = round(statistics.median(per) * 1e3, 2)
         out["steps"] = info["steps"]
         out[f"{coll}_launches"] = info["launches_per_op"]  # the far fusable steps run as one launch
         del send, recv, S, R
@@ -248,17 +273,12 @@ def other_workloads(reps=50):
 
         for _ in range(5):
             pat.check(op())
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(reps):
-            pat.check(op())
-        e1.record(stream)
-        torch.cuda.synchronize()
+        mean_ms, per = time_pair_and_reps(op, stream, reps)
         pat.check(pat.pat_check_device_status(stream))
-        sec = e0.elapsed_time(e1) / 1e3 / reps
+        sec = mean_ms / 1e3
         st, info = pat.pat_plan_info(code, n, count, dtype)
-        rows.append({"workload": desc, "us": round(sec * 1e6, 2), "steps": info["steps"],
+        rows.append({"workload": desc, "us": round(sec * 1e6, 2), "median_us": round(statistics.median(per) * 1e3, 2),
+                     "steps": info["steps"],
                      "launches": info["launches_per_op"],
                      "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
                      "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
@@ -445,34 +465,153 @@ def size_sweep(n=128, max_input_bytes=16 << 30, reps_bytes=32 << 30):
                       "rows": rows}), flush=True)
 
 
-def copy_probe(nbytes, reps):
-    """A plain device-to-device copy of known size: reads and writes nbytes."""
+def copy_probe(nbytes, reps, kind="torch"):
+    """A plain device-to-device copy of known size: reads and writes nbytes.
+    kind "torch": torch's copy (the runtime's __amd_rocclr_copyBuffer);
+    kind "nt": the nontemporal 16-byte-per-lane copy of libpatceiling.so, the
+    access type of the step kernels on large operations."""
+    import ctypes
+
     import torch
     n = nbytes // 2
     src = torch.ones(n, dtype=torch.bfloat16, device="cuda:0")
     dst = torch.empty_like(src)
-    dst.copy_(src)
+    stream = torch.cuda.current_stream()
+    if kind == "nt":
+        lib = ctypes.CDLL(os.path.join(ROOT, "paper_2506_20252_amd", "libpatceiling.so"))
+        lib.pat_ceiling_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        lib.pat_ceiling_copy.restype = ctypes.c_int
+
+        def op():
+            if lib.pat_ceiling_copy(src.data_ptr(), dst.data_ptr(), 2 * n, stream.cuda_stream) != 0:
+                raise RuntimeError("copy probe launch failed")
+    else:
+        def op():
+            dst.copy_(src)
+    op()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
+    e0.record(stream)
     for _ in range(reps):
-        dst.copy_(src)
-    e1.record()
+        op()
+    e1.record(stream)
     torch.cuda.synchronize()
+    if not bool(torch.equal(dst[:1 << 20], src[:1 << 20])):
+        raise RuntimeError("copy probe: wrong copy")
     ms = e0.elapsed_time(e1) / reps
-    print(json.dumps({"copy_bytes": 2 * n, "read_bytes": 2 * n, "write_bytes": 2 * n, "ms": round(ms, 4),
-                      "GBps_read_plus_write": round(4 * n / ms / 1e6, 1)}), flush=True)
+    print(json.dumps({"kind": kind, "copy_bytes": 2 * n, "read_bytes": 2 * n, "write_bytes": 2 * n,
+                      "ms": round(ms, 4), "GBps_read_plus_write": round(4 * n / ms / 1e6, 1)}), flush=True)
+
+
+def time_ops(op, stream, reps):
+    """Runs `op` reps times back to back on `stream` with a HIP event recorded
+    before the first and after each one.  Returns (mean ms per operation over
+    the whole run, list of per-operation ms)."""
+    import torch
+
+    from paper_2506_20252_amd import pat
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for k in range(reps):
+        pat.check(op(), "timed")
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [evs[k].elapsed_time(evs[k + 1]) for k in range(reps)]
+    return evs[0].elapsed_time(evs[-1]) / reps, per
+
+
+def time_pair_and_reps(op, stream, reps):
+    """For short operations: the mean over `reps` back-to-back operations
+    under one event pair (no events between them), then a second run of
+    `reps` with an event after each one for the per-operation times."""
+    import torch
+
+    from paper_2506_20252_amd import pat
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        pat.check(op())
+    e1.record(stream)
+    torch.cuda.synchronize()
+    _, per = time_ops(op, stream, reps)
+    return e0.elapsed_time(e1) / reps, per
+
+
+def kernel_name(coll, dtype, path, streaming, kind):
+    """The kernel template a launch runs (as rocprofv3 names it, abridged)."""
+    if coll == "rs":
+        traits = {"int32": "TI32", "float32": "TF32", "bfloat16": "TB16"}[dtype] + {0: "S", 1: "V", 2: "U"}[path]
+        op = f"RsOp<{traits}, {'true' if streaming else 'false'}>"
+    else:
+        op = {0: "AgOp<element>", 1: "AgOp<v4u>", 2: "AgOp<v4u, relaxed>"}[path]
+        op = op[:-1] + f", nontemporal={'true' if streaming else 'false'}>"
+    return ("tree_kernel<" if kind == 1 else "step_kernel<") + op + ">"
+
+
+def kernel_roofline(op, info, coll, dtype, reps=3):
+    """The traced pass: `reps` operations with a HIP event pair around every
+    kernel launch, recorded by the library on the kernels' stream, and each
+    launch's algorithmic bytes from the plan's byte model.  The dominant kernel
+    is the one with the most traced time; its rate is its launches' bytes
+    over their summed durations."""
+    import torch
+
+    from paper_2506_20252_amd import pat
+    launches = info["launches_per_op"]
+    pat.check(pat.pat_trace_start(reps * launches))
+    for _ in range(reps):
+        pat.check(op(), "traced")
+    torch.cuda.synchronize()
+    st, rows = pat.pat_trace_read(reps * launches)
+    pat.check(st, "pat_trace_read")
+    if len(rows) != reps * launches:
+        raise RuntimeError(f"trace: {len(rows)} launches recorded, {reps * launches} expected")
+    by = {}
+    for ms, nbytes, kind, _step in rows:
+        g = by.setdefault(kind, {"ms": 0.0, "bytes": 0.0, "launches": 0, "rates": []})
+        g["ms"] += ms
+        g["bytes"] += nbytes
+        g["launches"] += 1
+        g["rates"].append(nbytes / (ms / 1e3) / 1e9 if ms > 0 else 0.0)
+    op_bytes = sum(r[1] for r in rows) / reps
+    if abs(op_bytes - info["alg_bytes"]) > 1e-6 * info["alg_bytes"]:
+        raise RuntimeError(f"trace bytes per operation {op_bytes} != plan {info['alg_bytes']}")
+    dom = max(by, key=lambda k: by[k]["ms"])
+    g = by[dom]
+    achieved = g["bytes"] / (g["ms"] / 1e3) / 1e9
+    rates = sorted(g["rates"])
+    kinds = [{"kernel": kernel_name(coll, dtype, info["vector_path"], info["streaming"], k),
+              "launches_per_op": v["launches"] // reps, "bytes_per_launch": round(v["bytes"] / v["launches"], 1),
+              "avg_launch_us": round(v["ms"] / v["launches"] * 1e3, 3),
+              "frac": round(v["bytes"] / (v["ms"] / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)} for k, v in sorted(by.items())]
+    return {
+        "kernel": kernel_name(coll, dtype, info["vector_path"], info["streaming"], dom),
+        "achieved": achieved,
+        "launches_per_op": g["launches"] // reps,
+        "avg_launch_us": round(g["ms"] / g["launches"] * 1e3, 3),
+        "bytes_per_launch": round(g["bytes"] / g["launches"], 1),
+        "share_of_traced_time": round(g["ms"] / sum(v["ms"] for v in by.values()), 4),
+        "launch_frac": {"min": round(rates[0] / HBM_PEAK_GBPS, 4),
+                        "median": round(statistics.median(rates) / HBM_PEAK_GBPS, 4),
+                        "max": round(rates[-1] / HBM_PEAK_GBPS, 4)},
+        "traced_ops": reps,
+        "timing": "HIP event pair around each launch on the kernels' stream (library launch trace)",
+        "kernels": kinds,
+    }
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--mode", default="stream", choices=["persistent", "graph", "stream"])
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="instead: time a plain device copy of BYTES (the achievable-bandwidth line, and "
                          "the calibration kernel for the memory-traffic counters)")
+    ap.add_argument("--copy-probe-kind", default="torch", choices=["torch", "nt"])
     ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -491,7 +630,7 @@ def main():
     import torch
 
     if args.copy_probe:
-        copy_probe(args.copy_probe, args.steps)
+        copy_probe(args.copy_probe, args.steps, args.copy_probe_kind)
         return
     if args.budget_sweep:
         budget_sweep(args.workload, args.steps)
@@ -539,26 +678,20 @@ def main():
     torch.cuda.synchronize()
     pat.check(pat.pat_check_device_status(stream))
 
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        pat.check(op(), "timed")
-    end.record(stream)
-    torch.cuda.synchronize()
+    ms, rep_ms = time_ops(op, stream, args.steps)
     pat.check(pat.pat_check_device_status(stream))
-    ms = start.elapsed_time(end) / args.steps
     sec = ms / 1e3
-
     bus_per_rank = info["bus_bytes_per_rank"]
-    launches = 1 if args.mode == "persistent" else info["launches_per_op"]
-    alg_per_launch = info["alg_bytes"] / launches
-    launch_sec = sec / launches
-    achieved = alg_per_launch / launch_sec / 1e9
     traffic = committed_traffic(args.workload, args.mode)
-    kernel = ("persistent_kernel" if args.mode == "persistent" else "step_kernel") + \
-        ("<reduce-scatter>" if coll == "rs" else "<all-gather>")
+    if args.mode == "stream":
+        roof = kernel_roofline(op, info, coll, dtype)
+    else:
+        # no per-launch trace in these modes: the operation's time spread over its launches
+        launches = 1 if args.mode == "persistent" else info["launches_per_op"]
+        roof = {"kernel": "persistent_kernel" if args.mode == "persistent" else "step_kernel",
+                "achieved": info["alg_bytes"] / launches / (sec / launches) / 1e9, "launches_per_op": launches,
+                "timing": "operation time / launches (no per-launch trace in this mode)"}
+    achieved = roof.pop("achieved")
 
     out = {
         "metric": METRIC,
@@ -568,6 +701,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "median_ms_per_step": round(statistics.median(rep_ms), 4),
+        "rep_ms": {"min": round(min(rep_ms), 4), "max": round(max(rep_ms), 4), "reps": len(rep_ms)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -584,27 +719,28 @@ def main():
         "latency_us": round(ms * 1e3, 2),
         "alg_bytes_per_op": info["alg_bytes"],
         "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4),
-        "roofline": {"bound": "hbm", "kernel": kernel, "launches_per_op": launches,
-                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, **roof},
     }
     if not args.no_latency:
         out["small_size_latency"] = small_size_latency()
         out["other_workloads"] = other_workloads()
     if not args.no_cpu_baseline:
-        # The oracle's inputs: the first m positions of every chunk of the
-        # generator-filled send buffers (the collective only reads them).
-        import numpy as np
+        if coll == "rs":
+            out["cpu_baseline"] = cpu_baseline_rs(args.workload)
+        else:
+            # The oracle's inputs: the first m positions of every chunk of the
+            # generator-filled send buffers (the collective only reads them).
+            import numpy as np
 
-        def sample_inputs(m):
-            view = send.view(n, n, count) if coll == "rs" else send
-            part = view[..., :m].contiguous()
-            if dtype == "bfloat16":
-                return part.view(torch.int16).cpu().numpy().view(np.uint16)
-            return part.cpu().numpy()
+            def sample_inputs(m):
+                part = send[..., :m].contiguous()
+                if dtype == "bfloat16":
+                    return part.view(torch.int16).cpu().numpy().view(np.uint16)
+                return part.cpu().numpy()
 
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds, sample_inputs, min(count, 1 << 20))
+            out["cpu_baseline"] = cpu_baseline_ag(args.workload, args.cpu_seconds, sample_inputs,
+                                                  min(count, 1 << 20))
     del send, recv, sends, recvs
     torch.cuda.empty_cache()
     if not args.no_ceiling:

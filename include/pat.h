@@ -266,6 +266,25 @@ pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat
                             int32_t* a, int32_t* b, int32_t* c, int max_entries, int* nsteps,
                             int* nentries);
 
+/*
+ * Launch tracing, for measurement (stream mode only; graph and persistent
+ * modes and pat_reducescatter_noalloc record nothing).  pat_trace_start
+ * creates 2 * max_launches HIP events and arms the trace: the following
+ * operations record one event on their stream right before and one right
+ * after each kernel launch, until max_launches launches are recorded.
+ * pat_trace_read waits for the recorded events and returns, per launch in
+ * launch order: its duration in milliseconds (ms), the algorithmic bytes it
+ * moves by the plan's byte model (bytes; summed over an operation's launches
+ * they give pat_plan_info's alg_bytes), its kernel (kind: 0 one step, 1 a
+ * fused range of steps) and its first launch-level step (step).  Any output
+ * array may be NULL; each must hold `max` entries.  *n gets the number of
+ * launches recorded; if it exceeds max, PAT_ERR_INVALID_ARGUMENT and the trace
+ * stays armed.  Otherwise the events are destroyed and the trace disarmed.
+ * max_launches: 1 .. 2^20.
+ */
+pat_status_t pat_trace_start(int max_launches);
+pat_status_t pat_trace_read(float* ms, double* bytes, int32_t* kind, int32_t* step, int max, int* n);
+
 /* Cached plans: their number and the device memory they hold, all devices.
  * Plans are cached per (operation, nranks, count, dtype, budget, linear
  * order, device).  When a new plan would take a device's cached plans past

@@ -586,22 +586,73 @@ pat::TreeRange tree_range(const HostPlan& h, int vi) {
   return tr;
 }
 
+// Launch tracing (pat_trace_start / pat_trace_read): a HIP event pair around
+// each kernel launch of stream-mode operations, with the launch's algorithmic
+// bytes, until `max` launches are recorded.  Guarded by g_mu.
+struct Trace {
+  bool armed = false;
+  int max = 0, used = 0;
+  std::vector<hipEvent_t> ev;  // [2 * max]: before / after launch j
+  std::vector<double> bytes;   // [max]
+  std::vector<int32_t> kind;   // [max]: 0 step kernel, 1 fused range
+  std::vector<int32_t> step;   // [max]: launch-level step (the first of a fused range)
+
+  void clear() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+    ev.clear();
+    bytes.clear();
+    kind.clear();
+    step.clear();
+    armed = false;
+    max = used = 0;
+  }
+};
+Trace g_trace;
+
+// Algorithmic bytes of launch-level step s (a schedule step of one piece).
+double launch_bytes(const HostPlan& h, int vi, int s) {
+  const pat::PlanDesc& d = h.desc;
+  const int nexec = (int)d.exec.size();
+  const int64_t e0 = h.steps[vi][s].e0;
+  return pat::step_bytes(d, s % nexec, std::min<int64_t>(d.piece_elems, d.count - e0));
+}
+
 // Stream-mode launch sequence: one kernel per step, except that the fused
 // range (steps whose slot entries each serve one tree) runs as one launch.
+// With a trace, each launch is bracketed by its event pair on `q`.
 hipError_t enqueue_stream(const HostPlan& h, int coll, pat_dtype_t dt, int vi, const pat::KCtx& cx,
-                          const pat::TreeRange& tr, hipStream_t q) {
+                          const pat::TreeRange& tr, hipStream_t q, Trace* trace = nullptr) {
   const pat::Variant var = variant_for(coll, dt, vi);
   const auto& steps = h.steps[vi];
   const bool fuse = tr.s1 > tr.s0;
   for (int s = 0; s < (int)steps.size(); ++s) {
-    if (fuse && s == tr.s0) {
-      const hipError_t e = pat::launch_tree(var, h.streaming, cx, tr, q);
+    const bool traced = trace && trace->used < trace->max;
+    if (traced) {
+      const hipError_t e = hipEventRecord(trace->ev[2 * trace->used], q);
       if (e != hipSuccess) return e;
-      s = tr.s1 - 1;
-      continue;
     }
-    const hipError_t e = pat::launch_step(var, h.streaming, xcd_grain(h.xcd_run), cx, steps[s], q);
+    const int first = s;
+    double bytes = 0.0;
+    hipError_t e;
+    if (fuse && s == tr.s0) {
+      e = pat::launch_tree(var, h.streaming, cx, tr, q);
+      for (int k = tr.s0; k < tr.s1; ++k) bytes += launch_bytes(h, vi, k);
+      s = tr.s1 - 1;
+    } else {
+      e = pat::launch_step(var, h.streaming, xcd_grain(h.xcd_run), cx, steps[s], q);
+      bytes = launch_bytes(h, vi, s);
+    }
     if (e != hipSuccess) return e;
+    if (traced) {
+      const int j = trace->used;
+      e = hipEventRecord(trace->ev[2 * j + 1], q);
+      if (e != hipSuccess) return e;
+      trace->bytes[j] = bytes;
+      trace->kind[j] = fuse && first == tr.s0 ? 1 : 0;
+      trace->step[j] = first;
+      trace->used = j + 1;
+    }
   }
   return hipSuccess;
 }
@@ -689,7 +740,7 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   } else {
     const pat::TreeRange tr = tree_range(h, vi);
     if (mode == PAT_EXEC_STREAM) {
-      HIP_TRY(enqueue_stream(h, coll, dt, vi, cx, tr, stream));
+      HIP_TRY(enqueue_stream(h, coll, dt, vi, cx, tr, stream, g_trace.armed ? &g_trace : nullptr));
     } else {
       hipGraphExec_t& exec = plan->graphs[std::make_tuple(vi, cx.own_copy, tr.s0, tr.s1)];
       if (!exec) {
@@ -984,6 +1035,57 @@ pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat
     if (b) b[j] = d.entries[j].b;
     if (c) c[j] = d.entries[j].c;
   }
+  return PAT_OK;
+}
+
+pat_status_t pat_trace_start(int max_launches) {
+  if (max_launches < 1 || max_launches > (1 << 20)) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_trace.clear();
+  g_trace.ev.assign(2 * size_t(max_launches), nullptr);
+  // Timing-only events: without the system-scope fence an event record costs
+  // no cache writeback, which would otherwise sit between the traced kernels.
+  for (auto& e : g_trace.ev) {
+    const hipError_t err = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
+    if (err != hipSuccess) {
+      g_last_hip.store((int)err);
+      g_trace.clear();
+      return PAT_ERR_HIP;
+    }
+  }
+  g_trace.bytes.assign(max_launches, 0.0);
+  g_trace.kind.assign(max_launches, 0);
+  g_trace.step.assign(max_launches, 0);
+  g_trace.max = max_launches;
+  g_trace.armed = true;
+  return PAT_OK;
+}
+
+pat_status_t pat_trace_read(float* ms, double* bytes, int32_t* kind, int32_t* step, int max, int* n) {
+  if (!n) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (!g_trace.armed) {
+    *n = 0;
+    return PAT_ERR_INVALID_ARGUMENT;
+  }
+  const int used = g_trace.used;
+  *n = used;
+  if (used > max) return PAT_ERR_INVALID_ARGUMENT;  // still armed: call again with room for n
+  for (int j = 0; j < used; ++j) {
+    float t = 0.0f;
+    hipError_t e = hipEventSynchronize(g_trace.ev[2 * j + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, g_trace.ev[2 * j], g_trace.ev[2 * j + 1]);
+    if (e != hipSuccess) {
+      g_last_hip.store((int)e);
+      g_trace.clear();
+      return PAT_ERR_HIP;
+    }
+    if (ms) ms[j] = t;
+    if (bytes) bytes[j] = g_trace.bytes[j];
+    if (kind) kind[j] = g_trace.kind[j];
+    if (step) step[j] = g_trace.step[j];
+  }
+  g_trace.clear();
   return PAT_OK;
 }
 

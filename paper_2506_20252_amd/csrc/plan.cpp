@@ -214,23 +214,35 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, in
   return true;
 }
 
-double algorithmic_bytes(const PlanDesc& d) {
-  const double N = d.N;
-  if (d.count == 0) return 0.0;
-  if (d.N == 1) return 2.0 * double(d.count) * d.esize_in;  // a copy
-  double per_elem = 0.0;  // bytes per element of a chunk, summed over one rank's entries
+double step_bytes(const PlanDesc& d, int s, int64_t elems) {
+  if (d.N <= 1 || elems <= 0 || s < 0 || s >= (int)d.exec.size()) return 0.0;
   const double ei = d.esize_in, es = d.esize_slot;
-  if (d.coll == 0) {
-    for (const auto& e : d.entries) per_elem += ei + ei + (e.b >= 0 ? ei : 0.0);
-    per_elem += ei;  // the own chunk's copy into the receive buffer
-  } else {
-    for (const auto& e : d.entries) {
+  double per_elem = 0.0;  // bytes per element of a chunk, over one rank's entries of this step
+  const StepSpec& st = d.exec[s];
+  for (int j = 0; j < st.k; ++j) {
+    const DevEntry& e = d.entries[st.first + j];
+    if (d.coll == 0) {
+      per_elem += ei + ei + (e.b >= 0 ? ei : 0.0);
+    } else {
       per_elem += (e.a == kUser) ? ei : es;
       per_elem += (e.b == kUser) ? ei : es;
       per_elem += (e.c == kRootFinal) ? ei : es;
     }
   }
-  return N * per_elem * double(d.count);
+  if (d.coll == 0 && s == 0) per_elem += ei;  // the own chunk's copy into the receive buffer
+  return double(d.N) * per_elem * double(elems);
+}
+
+double algorithmic_bytes(const PlanDesc& d) {
+  if (d.count == 0) return 0.0;
+  if (d.N == 1) return 2.0 * double(d.count) * d.esize_in;  // a copy
+  double total = 0.0;
+  for (int piece = 0; piece < d.pieces; ++piece) {
+    const int64_t e0 = int64_t(piece) * d.piece_elems;
+    const int64_t len = std::min<int64_t>(d.piece_elems, d.count - e0);
+    for (int s = 0; s < (int)d.exec.size(); ++s) total += step_bytes(d, s, len);
+  }
+  return total;
 }
 
 }  // namespace pat

@@ -92,4 +92,10 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, in
 // receiver's own input or accumulator, write the accumulator.
 double algorithmic_bytes(const PlanDesc& d);
 
+// The same byte model for one step of one piece: step s of d.exec over a
+// piece of `elems` elements per chunk, all N ranks (all-gather: the own
+// chunk's copy counts in the first step).  Summed over every step and piece
+// it gives algorithmic_bytes(d).
+double step_bytes(const PlanDesc& d, int s, int64_t elems);
+
 }  // namespace pat

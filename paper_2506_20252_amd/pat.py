@@ -58,7 +58,8 @@ EXPORTS = (
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
     "pat_set_top_fusion", "pat_get_top_fusion",
     "pat_set_barrier_timeout_us", "pat_plan_info",
-    "pat_plan_steps", "pat_cache_stats", "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
+    "pat_plan_steps", "pat_trace_start", "pat_trace_read", "pat_cache_stats", "pat_check_device_status",
+    "pat_last_hip_error", "pat_status_string",
     "pat_finalize",
 )
 
@@ -117,6 +118,9 @@ def lib():
             "pat_plan_steps": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, _I32P, _I32P,
                                 ctypes.c_int, _I32P, _I32P, _I32P, _I32P, ctypes.c_int,
                                 ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
+            "pat_trace_start": ([ctypes.c_int], ctypes.c_int),
+            "pat_trace_read": ([ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double), _I32P, _I32P,
+                                ctypes.c_int, ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
             "pat_cache_stats": ([ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "pat_check_device_status": ([_P], ctypes.c_int),
             "pat_last_hip_error": ([], ctypes.c_int),
@@ -328,6 +332,22 @@ def pat_plan_steps(coll, nranks, count, dtype):
     steps = [(d[i], k[i]) for i in range(ns.value)]
     entries = [(pos[j], a[j], b[j], c[j]) for j in range(ne.value)]
     return st, steps, entries
+
+
+def pat_trace_start(max_launches):
+    return lib().pat_trace_start(int(max_launches))
+
+
+def pat_trace_read(max_launches):
+    """Returns (status, launches): launches = [(ms, bytes, kind, step)] in launch order."""
+    m = max(int(max_launches), 1)
+    ms, by = (ctypes.c_float * m)(), (ctypes.c_double * m)()
+    kind, step = (ctypes.c_int32 * m)(), (ctypes.c_int32 * m)()
+    n = ctypes.c_int()
+    st = lib().pat_trace_read(ms, by, kind, step, m, ctypes.byref(n))
+    if st != PAT_OK:
+        return st, []
+    return st, [(ms[j], by[j], kind[j], step[j]) for j in range(n.value)]
 
 
 def pat_cache_stats():

@@ -700,6 +700,39 @@ def test_tensor_wrappers_default_to_the_current_stream():
     np.testing.assert_array_equal(as_bits(ag_snap), np.broadcast_to(want[n - 1], (n, count)))
 
 
+@pytest.mark.parametrize("n,count,dtype,coll", [(1000, 64, "float32", "rs"), (24, 32768, "bfloat16", "ag"),
+                                                  (64, 4096, "float32", "rs"), (13, 1001, "bfloat16", "rs")])
+def test_launch_trace_covers_every_launch(n, count, dtype, coll):
+    """pat_trace_start / pat_trace_read: one event pair per kernel launch of
+    the traced operations, in launch order, whose bytes add up to the plan's
+    algorithmic bytes per operation; the traced results stay exact."""
+    pat.check(pat.pat_set_exec_mode("stream"))
+    code = pat.PAT_REDUCESCATTER if coll == "rs" else pat.PAT_ALLGATHER
+    st, info = pat.pat_plan_info(code, n, count, dtype)
+    launches = info["launches_per_op"]
+    pat.check(pat.pat_trace_start(2 * launches + 1))
+    seed = 0x7ACE + n
+    if coll == "rs":
+        got = run_rs(n, count, dtype, seed, mode="stream")
+        got2 = run_rs(n, count, dtype, seed, mode="stream")
+        check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed), dtype, oracle_t(code, n, count, dtype))
+    else:
+        got, host_in = run_ag(n, count, dtype, seed, mode="stream")
+        got2, _ = run_ag(n, count, dtype, seed, mode="stream")
+        np.testing.assert_array_equal(got, D.allgather(host_in))
+    np.testing.assert_array_equal(got, got2)
+    assert pat.pat_trace_read(1)[0] == pat.PAT_ERR_INVALID_ARGUMENT  # too small: stays armed
+    st, rows = pat.pat_trace_read(2 * launches + 1)
+    pat.check(st)
+    assert len(rows) == 2 * launches
+    for op in (rows[:launches], rows[launches:]):
+        assert sum(r[1] for r in op) == pytest.approx(info["alg_bytes"], rel=1e-9)
+        assert all(r[0] > 0 for r in op)
+        assert [r[3] for r in op] == sorted(r[3] for r in op)  # launch order
+        assert sum(r[2] for r in op) == (1 if info["fused_steps"] else 0)
+    assert pat.pat_trace_read(4)[0] == pat.PAT_ERR_INVALID_ARGUMENT  # disarmed
+
+
 def test_pointer_checks_follow_every_argument():
     """The per-pointer checks are skipped only for the exact pointer set a
     thread last validated with the same operation, rank count, count and
