@@ -102,14 +102,15 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def committed_traffic(workload_id, mode):
-    """HBM bytes per launch of the step kernel from the committed counter
-    summary, if it was taken on the current kernel source; else None.  Stream
-    and graph modes launch the same step kernels; the persistent kernel has no
-    summary."""
+def committed_traffic(workload_id, mode, kernel):
+    """HBM-side bytes per launch of `kernel` (step_kernel / tree_kernel) from
+    the committed counter summary, if it was taken on the current kernel
+    source; else None.  Stream and graph modes launch the same kernels; the
+    persistent kernel has no summary."""
     if mode == "persistent":
         return None
-    path = os.path.join(ROOT, "profiles", f"traffic_step_kernel_workload{workload_id}.txt")
+    kind = "tree_kernel" if kernel.startswith("tree_kernel") else "step_kernel"
+    path = os.path.join(ROOT, "profiles", f"traffic_{kind}_workload{workload_id}.txt")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -602,6 +603,67 @@ def kernel_roofline(op, info, coll, dtype, reps=3):
     }
 
 
+def step_clock_report(wid, reps=5):
+    """The fused launch of one workload, step by step: with PAT_STEP_CLOCK=1
+    the fused kernel records the device wall clock per workgroup before its
+    first step and after each one.  Reports, per fused step, its distance,
+    chunks per rank, algorithmic bytes and the median / 90th percentile over
+    workgroups of its duration, and the launch's first-to-last stamp span
+    (the last of `reps` operations)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    coll, n, count, dtype, dist, seed, desc = WORKLOADS[wid]
+    tdt = {"int32": torch.int32, "float32": torch.float32, "bfloat16": torch.bfloat16}[dtype]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    pat.check(pat.pat_set_exec_mode("stream"))
+    if coll == "rs":
+        send, recv = torch.empty((n, n * count), dtype=tdt, device=dev), torch.empty((n, count), dtype=tdt, device=dev)
+        code = pat.PAT_REDUCESCATTER
+    else:
+        send, recv = torch.empty((n, count), dtype=tdt, device=dev), torch.empty((n, n * count), dtype=tdt, device=dev)
+        code = pat.PAT_ALLGATHER
+    for x in range(n):
+        synth.fill(send[x], dist, seed, x)
+    S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
+
+    def op():
+        if coll == "rs":
+            return pat.pat_reducescatter(S, R, count, dtype, pat.PAT_SUM, n, stream)
+        return pat.pat_allgather(S, R, count, dtype, n, stream)
+
+    st, info = pat.pat_plan_info(code, n, count, dtype)
+    pat.check(pat.pat_trace_start(reps * info["launches_per_op"]))
+    for _ in range(reps):
+        pat.check(op())
+    torch.cuda.synchronize()
+    st, launches = pat.pat_trace_read(reps * info["launches_per_op"])
+    pat.check(st)
+    st, stamps, tpu = pat.pat_step_clock(code, n, count, dtype)
+    pat.check(st, "pat_step_clock")
+    st, steps, entries = pat.pat_plan_steps(code, n, count, dtype)
+    fused = [r for r in launches[-info["launches_per_op"]:] if r[2] == 1]
+    s0 = fused[0][3] if fused else 0
+    dur = np.diff(stamps.astype(np.int64), axis=1) / tpu
+    rows = []
+    for k in range(dur.shape[1]):
+        d, kk = steps[s0 + k]
+        rows.append({"step": s0 + k, "distance": d, "chunks_per_rank": kk,
+                     "median_us": round(float(np.median(dur[:, k])), 3),
+                     "p90_us": round(float(np.percentile(dur[:, k], 90)), 3)})
+    print(json.dumps({"metric": "PAT fused launch, per-step device clock (median over workgroups)",
+                      "workload": desc, "workgroups": int(stamps.shape[0]), "fused_steps": dur.shape[1],
+                      "launch_us_event": round(fused[-1][0] * 1e3, 3) if fused else None,
+                      "launch_bytes": fused[-1][1] if fused else None,
+                      "span_us": round(float((stamps[:, -1].max() - stamps[:, 0].min()) / tpu), 3),
+                      "first_stamp_spread_us": round(float((stamps[:, 0].max() - stamps[:, 0].min()) / tpu), 3),
+                      "steps": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -619,6 +681,8 @@ def main():
     ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-ceiling probes")
     ap.add_argument("--budget-sweep", action="store_true",
                     help="instead: time the workload at every aggregation level (T = 1 .. full)")
+    ap.add_argument("--step-clock", action="store_true",
+                    help="instead: per-step device clock of the workload's fused launch (PAT_STEP_CLOCK=1)")
     ap.add_argument("--size-sweep", action="store_true",
                     help="instead: both collectives at N=128 over chunk sizes from 256 B (float32)")
     args = ap.parse_args()
@@ -637,6 +701,10 @@ def main():
         return
     if args.size_sweep:
         size_sweep()
+        return
+    if args.step_clock:
+        os.environ["PAT_STEP_CLOCK"] = "1"  # read when the plan is made
+        step_clock_report(args.workload)
         return
 
     import synth
@@ -682,7 +750,6 @@ def main():
     pat.check(pat.pat_check_device_status(stream))
     sec = ms / 1e3
     bus_per_rank = info["bus_bytes_per_rank"]
-    traffic = committed_traffic(args.workload, args.mode)
     if args.mode == "stream":
         roof = kernel_roofline(op, info, coll, dtype)
     else:
@@ -692,6 +759,7 @@ def main():
                 "achieved": info["alg_bytes"] / launches / (sec / launches) / 1e9, "launches_per_op": launches,
                 "timing": "operation time / launches (no per-launch trace in this mode)"}
     achieved = roof.pop("achieved")
+    traffic = committed_traffic(args.workload, args.mode, roof["kernel"])
 
     out = {
         "metric": METRIC,

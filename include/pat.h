@@ -285,6 +285,25 @@ pat_status_t pat_plan_steps(pat_collective_t coll, int nranks, size_t count, pat
 pat_status_t pat_trace_start(int max_launches);
 pat_status_t pat_trace_read(float* ms, double* bytes, int32_t* kind, int32_t* step, int max, int* n);
 
+/*
+ * Step clock of fused launches (measurement; stream mode).  When the
+ * environment variable PAT_STEP_CLOCK is 1 as a plan is made, every fused
+ * launch of that plan (the range of steps one workgroup per (tree, tile) runs
+ * with workgroup barriers in between) records, per workgroup, the device wall
+ * clock before its first step and after each step: step k of workgroup w took
+ * stamps[w * per_workgroup + k + 1] - stamps[w * per_workgroup + k] ticks
+ * (*ticks_per_us per microsecond).  pat_step_clock waits for the plan's last
+ * operation and copies the stamps of its last fused launch (the plan of the
+ * current device, buffer budget and linear order).  *workgroups and
+ * *per_workgroup are set whenever such stamps exist; `stamps` must hold
+ * their product (else PAT_ERR_INVALID_ARGUMENT).  PAT_ERR_INVALID_ARGUMENT
+ * too when the plan has none (no such plan, the variable was off, or no
+ * fused launch ran in stream mode).  Off by default: the fused kernel then
+ * records nothing.
+ */
+pat_status_t pat_step_clock(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype, uint64_t* stamps,
+                            size_t max, int* workgroups, int* per_workgroup, double* ticks_per_us);
+
 /* Cached plans: their number and the device memory they hold, all devices.
  * Plans are cached per (operation, nranks, count, dtype, budget, linear
  * order, device).  When a new plan would take a device's cached plans past

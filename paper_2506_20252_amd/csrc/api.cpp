@@ -238,6 +238,12 @@ struct Plan {
   hipEvent_t done = nullptr;  // recorded after the plan's last operation
   bool used = false;
   uint64_t last_use = 0;     // LRU stamp
+  // Step clock of fused launches (PAT_STEP_CLOCK=1 when the plan was made;
+  // stream mode): the last fused launch's per-workgroup stamps.
+  bool step_clock = false;
+  uint64_t* d_stamps = nullptr;
+  size_t stamps_cap = 0;      // entries
+  int stamp_wgs = 0, stamps_per_wg = 0;
 
   ~Plan() {
     for (auto& kv : graphs)
@@ -252,6 +258,7 @@ struct Plan {
     (void)hipFree(d_slots);
     (void)hipFree(d_rootacc);
     (void)hipFree(d_sync);
+    (void)hipFree(d_stamps);
   }
 };
 
@@ -439,6 +446,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
   HIP_TRY(hipHostMalloc((void**)&p->pinned, 2 * size_t(N) * sizeof(void*), hipHostMallocDefault));
   HIP_TRY(hipEventCreateWithFlags(&p->upload_done, hipEventDisableTiming));
   HIP_TRY(hipEventCreateWithFlags(&p->done, hipEventDisableTiming));
+  if (const char* e = std::getenv("PAT_STEP_CLOCK")) p->step_clock = e[0] == '1';
   if (const char* e = std::getenv("PAT_DEBUG")) {
     if (e[0] == '1') {
       std::fprintf(stderr,
@@ -739,6 +747,21 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
     HIP_TRY(pat::launch_persistent(var, nt, cx, grid, stream));
   } else {
     const pat::TreeRange tr = tree_range(h, vi);
+    if (mode == PAT_EXEC_STREAM && plan->step_clock && tr.s1 > tr.s0) {
+      const int wgs = N * (int)tr.tiles, per = tr.s1 - tr.s0 + 1;
+      const size_t need = size_t(wgs) * per;
+      if (plan->stamps_cap < need) {
+        HIP_TRY(hipStreamSynchronize(stream));
+        HIP_TRY(hipFree(plan->d_stamps));
+        plan->d_stamps = nullptr;
+        plan->stamps_cap = 0;
+        HIP_TRY(hipMalloc((void**)&plan->d_stamps, need * sizeof(uint64_t)));
+        plan->stamps_cap = need;
+      }
+      plan->stamp_wgs = wgs;
+      plan->stamps_per_wg = per;
+      cx.stamps = plan->d_stamps;
+    }
     if (mode == PAT_EXEC_STREAM) {
       HIP_TRY(enqueue_stream(h, coll, dt, vi, cx, tr, stream, g_trace.armed ? &g_trace : nullptr));
     } else {
@@ -1086,6 +1109,26 @@ pat_status_t pat_trace_read(float* ms, double* bytes, int32_t* kind, int32_t* st
     if (step) step[j] = g_trace.step[j];
   }
   g_trace.clear();
+  return PAT_OK;
+}
+
+pat_status_t pat_step_clock(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype, uint64_t* stamps,
+                            size_t max, int* workgroups, int* per_workgroup, double* ticks_per_us) {
+  if (!workgroups || !per_workgroup) return PAT_ERR_INVALID_ARGUMENT;
+  *workgroups = *per_workgroup = 0;
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  auto it = g_plans.find(PlanKey((int)coll, nranks, (int64_t)count, (int)dtype, budget_now(), order_now(), device));
+  if (it == g_plans.end() || !it->second->step_clock || it->second->stamp_wgs == 0) return PAT_ERR_INVALID_ARGUMENT;
+  Plan* p = it->second.get();
+  *workgroups = p->stamp_wgs;
+  *per_workgroup = p->stamps_per_wg;
+  if (ticks_per_us) *ticks_per_us = double(p->clock_khz) / 1000.0;
+  const size_t need = size_t(p->stamp_wgs) * p->stamps_per_wg;
+  if (!stamps || max < need) return PAT_ERR_INVALID_ARGUMENT;
+  if (p->used) HIP_TRY(hipEventSynchronize(p->done));
+  HIP_TRY(hipMemcpy(stamps, p->d_stamps, need * sizeof(uint64_t), hipMemcpyDeviceToHost));
   return PAT_OK;
 }
 

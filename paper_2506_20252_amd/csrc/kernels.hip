@@ -836,18 +836,26 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int
 // tree c, over the same tile: by this workgroup.
 // A workgroup barrier between steps then replaces the kernel boundary; each
 // wave first waits for its own stores.
+//
+// With cx.stamps set (measurement only), lane 0 records the device wall clock
+// before the first step and after each step's barrier (the last step gets a
+// barrier of its own then), so that step k of this workgroup took
+// stamps[k + 1] - stamps[k] ticks.
 template <class Op>
 __global__ __launch_bounds__(kTreeThreads) void tree_kernel(KCtx cx, TreeRange tr) {
   const int c = (int)(blockIdx.x / tr.tiles);
   const int64_t tile = (int64_t)blockIdx.x - (int64_t)c * tr.tiles;
   const int64_t t0 = tile * tr.tile_vecs;
+  uint64_t* const stamp = cx.stamps ? cx.stamps + (int64_t)blockIdx.x * (tr.s1 - tr.s0 + 1) : nullptr;
+  if (stamp && threadIdx.x == 0) stamp[0] = wall_clock64();
   for (int s = tr.s0; s < tr.s1; ++s) {
     const DevStep st = cx.steps[s];
     const int64_t left = st.V - t0;
     Op::tree_step(cx, st, c, t0, left < tr.tile_vecs ? left : tr.tile_vecs, tile == tr.tiles - 1);
-    if (s + 1 < tr.s1) {
+    if (s + 1 < tr.s1 || stamp) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
+      if (stamp && threadIdx.x == 0) stamp[s - tr.s0 + 1] = wall_clock64();
     }
   }
 }

@@ -36,6 +36,8 @@ struct KCtx {
                               // "ids taken", 32 "ids done" and one "shards done" counter, 128 B apart
                               // (zero between launches)
   unsigned* status;           // bit 0: a persistent kernel's wait timed out
+  uint64_t* stamps;           // fused launches, measurement only (null: off): per workgroup, the device
+                              // wall clock before its first step and after each step, (s1 - s0 + 1) apiece
 };
 
 // Words of the persistent kernel's counter area for `nsteps` launch-level steps.

@@ -58,8 +58,8 @@ EXPORTS = (
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
     "pat_set_top_fusion", "pat_get_top_fusion",
     "pat_set_barrier_timeout_us", "pat_plan_info",
-    "pat_plan_steps", "pat_trace_start", "pat_trace_read", "pat_cache_stats", "pat_check_device_status",
-    "pat_last_hip_error", "pat_status_string",
+    "pat_plan_steps", "pat_trace_start", "pat_trace_read", "pat_step_clock", "pat_cache_stats",
+    "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
     "pat_finalize",
 )
 
@@ -121,6 +121,9 @@ def lib():
             "pat_trace_start": ([ctypes.c_int], ctypes.c_int),
             "pat_trace_read": ([ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double), _I32P, _I32P,
                                 ctypes.c_int, ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
+            "pat_step_clock": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
+                                ctypes.POINTER(ctypes.c_uint64), ctypes.c_size_t, ctypes.POINTER(ctypes.c_int),
+                                ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
             "pat_cache_stats": ([ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "pat_check_device_status": ([_P], ctypes.c_int),
             "pat_last_hip_error": ([], ctypes.c_int),
@@ -348,6 +351,23 @@ def pat_trace_read(max_launches):
     if st != PAT_OK:
         return st, []
     return st, [(ms[j], by[j], kind[j], step[j]) for j in range(n.value)]
+
+
+def pat_step_clock(coll, nranks, count, dtype):
+    """Returns (status, stamps, ticks_per_us): stamps is a (workgroups,
+    steps + 1) numpy array of device wall-clock ticks of the plan's last fused
+    launch (PAT_STEP_CLOCK=1), or None."""
+    import numpy as np
+    wgs, per, tpu = ctypes.c_int(), ctypes.c_int(), ctypes.c_double()
+    st = lib().pat_step_clock(int(coll), int(nranks), int(count), _dtype(dtype), None, 0, ctypes.byref(wgs),
+                              ctypes.byref(per), ctypes.byref(tpu))
+    if wgs.value == 0:
+        return st, None, 0.0
+    out = np.zeros((wgs.value, per.value), dtype=np.uint64)
+    st = lib().pat_step_clock(int(coll), int(nranks), int(count), _dtype(dtype),
+                              out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), out.size, ctypes.byref(wgs),
+                              ctypes.byref(per), ctypes.byref(tpu))
+    return st, (out if st == PAT_OK else None), tpu.value
 
 
 def pat_cache_stats():

@@ -733,6 +733,40 @@ def test_launch_trace_covers_every_launch(n, count, dtype, coll):
     assert pat.pat_trace_read(4)[0] == pat.PAT_ERR_INVALID_ARGUMENT  # disarmed
 
 
+@pytest.mark.parametrize("n,count,dtype,coll", [(1000, 64, "float32", "rs"), (1000, 64, "float32", "ag"),
+                                                  (24, 32768, "bfloat16", "ag"), (6, 1024, "int32", "rs")])
+def test_step_clock_of_fused_launches(n, count, dtype, coll, monkeypatch):
+    """PAT_STEP_CLOCK=1: the fused kernel records, per workgroup, one stamp
+    before its first step and one after each, never decreasing; the result
+    stays exact; with the variable off nothing is recorded."""
+    code = pat.PAT_REDUCESCATTER if coll == "rs" else pat.PAT_ALLGATHER
+    st, info = pat.pat_plan_info(code, n, count, dtype)
+    assert info["fused_steps"] >= 2
+    pat.check(pat.pat_finalize())
+    monkeypatch.setenv("PAT_STEP_CLOCK", "1")
+    seed = 0xC10C + n
+    try:
+        if coll == "rs":
+            got = run_rs(n, count, dtype, seed, mode="stream")
+            check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed), dtype, oracle_t(code, n, count, dtype))
+        else:
+            got, host_in = run_ag(n, count, dtype, seed, mode="stream")
+            np.testing.assert_array_equal(got, D.allgather(host_in))
+        st, stamps, tpu = pat.pat_step_clock(code, n, count, dtype)
+        pat.check(st, "pat_step_clock")
+        assert stamps.shape[1] == info["fused_steps"] + 1 and stamps.shape[0] % n == 0
+        assert (np.diff(stamps.astype(np.int64), axis=1) >= 0).all() and (stamps[:, 0] > 0).all()
+        assert 1.0 <= tpu <= 10000.0
+    finally:
+        monkeypatch.delenv("PAT_STEP_CLOCK")
+        pat.check(pat.pat_finalize())
+    if coll == "rs":
+        run_rs(n, count, dtype, seed, mode="stream")
+    else:
+        run_ag(n, count, dtype, seed, mode="stream")
+    assert pat.pat_step_clock(code, n, count, dtype)[0] == pat.PAT_ERR_INVALID_ARGUMENT
+
+
 def test_pointer_checks_follow_every_argument():
     """The per-pointer checks are skipped only for the exact pointer set a
     thread last validated with the same operation, rank count, count and
