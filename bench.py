@@ -402,6 +402,7 @@ def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
         T *= 2
     pat.check(pat.pat_set_buffer_bytes(0))
     print(json.dumps({"metric": "PAT budget sweep (steps and time per aggregation level)", "workload": desc,
+                      "exec_mode": ["persistent", "graph", "stream", "dataflow"][pat.pat_get_exec_mode()],
                       "nranks": n, "log2_n": round(math.log2(n), 3), "rows": rows}), flush=True)
 
 
@@ -669,7 +670,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--mode", default="stream", choices=["persistent", "graph", "stream"])
+    ap.add_argument("--mode", default="stream", choices=["persistent", "graph", "stream", "dataflow"])
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="instead: time a plain device copy of BYTES (the achievable-bandwidth line, and "
                          "the calibration kernel for the memory-traffic counters)")
@@ -696,6 +697,8 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe, args.steps, args.copy_probe_kind)
         return
+    from paper_2506_20252_amd import pat as _pat
+    _pat.check(_pat.pat_set_exec_mode(args.mode))  # the sweeps run in the chosen mode too
     if args.budget_sweep:
         budget_sweep(args.workload, args.steps)
         return

@@ -95,7 +95,19 @@ typedef enum {
   /* One kernel per step, launched directly on the stream.  The default: as
    * fast as the graph for large operations, and without the graph launch's
    * fixed cost for small ones. */
-  PAT_EXEC_STREAM = 2
+  PAT_EXEC_STREAM = 2,
+  /* Dataflow: one launch per piece, no step barrier.  Workgroups take work
+   * in step order as in the persistent mode, but a work item (one tile of
+   * one chunk-edge) waits only for the two buffers it touches: per (rank,
+   * slot) counters of completed tiles -- the receiver's slot emptied by every
+   * earlier reader before it is refilled, the sender's slot filled before it
+   * is read (all-gather); the child's accumulator complete, the receiver's
+   * earlier additions done (reduce-scatter).  Ranks and trees run ahead of
+   * one another as far as their own buffers allow (section "Future work":
+   * the linear part).  Waits are bounded like the persistent mode's
+   * (PAT_ERR_TIMEOUT).  Needs N x (slot entries per rank + 1) 4-byte counters,
+   * at most 256 MiB (else PAT_ERR_UNSUPPORTED). */
+  PAT_EXEC_DATAFLOW = 3
 } pat_exec_mode_t;
 
 /*
@@ -180,7 +192,7 @@ pat_status_t pat_set_linear_order(int order);
 int pat_get_linear_order(void);
 
 /* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_STREAM, or the
- * PAT_EXEC_MODE environment variable (persistent | graph | stream). */
+ * PAT_EXEC_MODE environment variable (persistent | graph | stream | dataflow). */
 pat_status_t pat_set_exec_mode(int mode);
 int pat_get_exec_mode(void);
 

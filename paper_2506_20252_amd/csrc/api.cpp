@@ -45,6 +45,7 @@ int mode_now() {
   if (const char* e = std::getenv("PAT_EXEC_MODE")) {
     if (!std::strcmp(e, "persistent")) return PAT_EXEC_PERSISTENT;
     if (!std::strcmp(e, "graph")) return PAT_EXEC_GRAPH;
+    if (!std::strcmp(e, "dataflow")) return PAT_EXEC_DATAFLOW;
   }
   return PAT_EXEC_STREAM;
 }
@@ -244,6 +245,13 @@ struct Plan {
   uint64_t* d_stamps = nullptr;
   size_t stamps_cap = 0;      // entries
   int stamp_wgs = 0, stamps_per_wg = 0;
+  // Dataflow execution (made on first use): every step tiled, per path; the
+  // dependency table; per (rank, buffer) counters of completed tiles.
+  bool df_ready = false;
+  std::vector<pat::DevStep> df_steps[3];
+  pat::DevStep* d_df_steps[3] = {nullptr, nullptr, nullptr};
+  pat::DevDep* d_deps = nullptr;
+  unsigned* d_counters = nullptr;
 
   ~Plan() {
     for (auto& kv : graphs)
@@ -259,6 +267,9 @@ struct Plan {
     (void)hipFree(d_rootacc);
     (void)hipFree(d_sync);
     (void)hipFree(d_stamps);
+    for (auto* p : d_df_steps) (void)hipFree(p);
+    (void)hipFree(d_deps);
+    (void)hipFree(d_counters);
   }
 };
 
@@ -505,6 +516,62 @@ struct CheckedPointers {
 };
 thread_local CheckedPointers t_checked;
 
+// Dataflow execution: work items per step for chunks of one tile or more.
+constexpr int64_t kDataflowItems = 4096;
+
+// Largest counter array dataflow execution allocates (N x (slot entries + 1)
+// words); beyond it the mode is refused with PAT_ERR_UNSUPPORTED.
+constexpr size_t kMaxDataflowCounters = size_t(256) << 20;
+
+// The dataflow tables of a plan, made on its first dataflow operation.
+pat_status_t ensure_dataflow(Plan* p, int coll, pat_dtype_t dt) {
+  if (p->df_ready) return PAT_OK;
+  const HostPlan& h = p->h;
+  const pat::PlanDesc& d = h.desc;
+  const size_t stride = size_t(d.slots.entries) + 1;
+  if (stride * d.N * sizeof(unsigned) > kMaxDataflowCounters) return PAT_ERR_UNSUPPORTED;
+  std::vector<pat::DevDep> deps;
+  if (!pat::dataflow_deps(d, &deps)) return PAT_ERR_INTERNAL;
+  for (int path = 0; path < 3; ++path) {
+    if (!h.has_path[path]) continue;
+    const pat::Variant v = variant_for(coll, dt, path);
+    const int pack = pat::variant_pack_tile(v);
+    if (!build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pack, path == 2 && pat::variant_partial(v),
+                     pat::variant_partial_items(v), &p->df_steps[path]))
+      return PAT_ERR_INTERNAL;
+    // Work items: whole edges, about four packed work items' worth of vectors
+    // and at most one edge per lane, for chunks under one tile; else runs of
+    // tiles of one edge, about kDataflowItems items per step.
+    for (auto& st : p->df_steps[path]) {
+      const int64_t edges = int64_t(d.N) * st.k;
+      if (st.tiles_per_edge == 0) {
+        st.df_edges = (int32_t)std::max<int64_t>(1, std::min<int64_t>(pat::kThreads, 4 * pack / std::max<int64_t>(1, st.V)));
+        st.df_tiles = 1;
+        st.items = (edges + st.df_edges - 1) / st.df_edges;
+      } else {
+        st.df_edges = 0;
+        st.df_tiles = (int32_t)std::max<int64_t>(
+            1, std::min<int64_t>(st.tiles_per_edge, (edges * st.tiles_per_edge + kDataflowItems - 1) / kDataflowItems));
+        st.items = edges * ((st.tiles_per_edge + st.df_tiles - 1) / st.df_tiles);
+      }
+    }
+  }
+  HIP_TRY(hipMalloc((void**)&p->d_deps, std::max<size_t>(1, deps.size()) * sizeof(pat::DevDep)));
+  if (!deps.empty())
+    HIP_TRY(hipMemcpy(p->d_deps, deps.data(), deps.size() * sizeof(pat::DevDep), hipMemcpyHostToDevice));
+  HIP_TRY(hipMalloc((void**)&p->d_counters, stride * d.N * sizeof(unsigned)));
+  HIP_TRY(hipMemset(p->d_counters, 0, stride * d.N * sizeof(unsigned)));
+  for (int path = 0; path < 3; ++path) {
+    if (p->df_steps[path].empty()) continue;
+    HIP_TRY(hipMalloc((void**)&p->d_df_steps[path], p->df_steps[path].size() * sizeof(pat::DevStep)));
+    HIP_TRY(hipMemcpy(p->d_df_steps[path], p->df_steps[path].data(),
+                      p->df_steps[path].size() * sizeof(pat::DevStep), hipMemcpyHostToDevice));
+  }
+  p->bytes += std::max<size_t>(1, deps.size()) * sizeof(pat::DevDep) + stride * d.N * sizeof(unsigned);
+  p->df_ready = true;
+  return PAT_OK;
+}
+
 // Argument checks shared by every entry point.  PAT_OK with *nothing set
 // when count == 0 (no pointer is examined then); *vec tells whether every
 // pointer is 16-byte aligned.
@@ -730,7 +797,39 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   const pat::Variant var = variant_for(coll, dt, vi);
   const auto& steps = h.steps[vi];
   const int mode = mode_now();
-  if (mode == PAT_EXEC_PERSISTENT) {
+  if (mode == PAT_EXEC_DATAFLOW) {
+    // The relaxed bf16 reduce-scatter gives partial vectors work items of
+    // their own, spanning many edges: dataflow runs its element-wide twin.
+    const int dvi = pat::variant_partial_items(var) ? 0 : vi;
+    const pat::Variant dvar = variant_for(coll, dt, dvi);
+    const pat_status_t ds = ensure_dataflow(plan, coll, dt);
+    if (ds != PAT_OK) return ds;
+    const bool nt = h.streaming;
+    int& capacity = plan->capacity[dvar][nt ? 1 : 0];
+    if (capacity == 0) HIP_TRY(pat::persistent_capacity(dvar, nt, &capacity));
+    const auto& dsteps = plan->df_steps[dvi];
+    const int nexec = (int)h.desc.exec.size();
+    int64_t most = 1;
+    for (const auto& st : dsteps) most = std::max(most, st.items);
+    int64_t cap = capacity;
+    const double per_step = h.alg_bytes / double(std::max<size_t>(1, dsteps.size()));
+    if (const int per_cu = blocks_per_cu_cap(per_step)) cap = std::min<int64_t>(cap, int64_t(per_cu) * plan->cus);
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cap, most));  // any size is safe
+    pat::KCtx dx = make_ctx(h, dvi, plan->d_send, plan->d_recv, plan->d_slots, plan->d_rootacc, plan->d_entries,
+                            plan->d_df_steps[dvi], count, N, own_copy);
+    dx.timeout_ticks = cx.timeout_ticks;
+    dx.queue = cx.queue;
+    dx.status = cx.status;
+    dx.deps = plan->d_deps;
+    dx.counters = plan->d_counters;
+    dx.counter_stride = int64_t(h.desc.slots.entries) + 1;
+    dx.nsteps = nexec;
+    for (int piece = 0; piece < h.desc.pieces; ++piece) {
+      dx.steps = plan->d_df_steps[dvi] + size_t(piece) * nexec;
+      const bool small = dsteps[size_t(piece) * nexec].tiles_per_edge == 0;  // a piece's steps share V
+      HIP_TRY(pat::launch_dataflow(dvar, nt, dx, small, grid, stream));
+    }
+  } else if (mode == PAT_EXEC_PERSISTENT) {
     const bool nt = h.streaming;
     int& capacity = plan->capacity[var][nt ? 1 : 0];
     if (capacity == 0) HIP_TRY(pat::persistent_capacity(var, nt, &capacity));
@@ -945,7 +1044,7 @@ size_t pat_get_buffer_bytes(void) {
 }
 
 pat_status_t pat_set_exec_mode(int mode) {
-  if (mode < PAT_EXEC_PERSISTENT || mode > PAT_EXEC_STREAM) return PAT_ERR_INVALID_ARGUMENT;
+  if (mode < PAT_EXEC_PERSISTENT || mode > PAT_EXEC_DATAFLOW) return PAT_ERR_INVALID_ARGUMENT;
   std::lock_guard<std::mutex> lock(g_mu);
   g_mode = mode;
   return PAT_OK;

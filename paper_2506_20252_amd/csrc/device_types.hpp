@@ -22,6 +22,20 @@ struct DevEntry {
   int32_t p, a, b, c;
 };
 
+// Dataflow execution: the two rank-relative counters one chunk-edge touches
+// (entry j of the step table).  Every rank's slot entry e (and, as entry
+// `entries`, its own chunk's accumulator) counts the completed tiles of the
+// edges that accessed it.  Access 1 is at rank r + o1, access 2 at r + o2
+// (all-gather: o1 = 0, the sender's source slot; o2 = d, the receiver's slot;
+// reduce-scatter: o1 = d, the child's partial; o2 = 0, the receiver's
+// accumulator).  e = -1: no counter.  Counters count completed tiles (1 per
+// whole edge for chunks under one tile); an edge may run once counter e has
+// reached need * (tiles per edge): every earlier access to that buffer, in
+// step order, is complete.
+struct DevDep {
+  int32_t e1, need1, e2, need2;
+};
+
 // One launch-level step (a schedule step of one piece), as the kernels see it.
 struct DevStep {
   int32_t d;               // distance: peer = r + d (all-gather) / child = r + d (reduce-scatter)
@@ -37,6 +51,9 @@ struct DevStep {
   int64_t tiles_per_edge;  // > 0: each work item is one tile of one edge; 0: items pack edges
   int64_t items;           // work items (workgroups) of this step; where they take the partial
                            // vectors, the last ceil(N * k / 256) give each edge's to a lane
+  int32_t df_edges;        // dataflow execution: whole edges per work item (chunks under one tile;
+                           // 0: the item is df_tiles tiles of one edge)
+  int32_t df_tiles;        // dataflow execution: tiles of one edge per work item
 };
 
 }  // namespace pat

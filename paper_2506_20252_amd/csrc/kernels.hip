@@ -235,6 +235,7 @@ __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st
 // may end in a partial vector, st.back elements short).
 template <typename Unit, int kU, bool NT, int kTU = kU, int kA = 0>
 struct AgOp {
+  static constexpr bool kGather = true;
   static constexpr int U = kU;
   static constexpr int TU = kTU;
   static constexpr int kTile = kThreads * TU;      // vectors of one tiled work item
@@ -521,6 +522,7 @@ struct TB16U : TB16V {
 
 template <class R, bool NT>
 struct RsOp {
+  static constexpr bool kGather = false;
   using in_t = typename R::in_t;
   using acc_t = typename R::acc_t;
   static constexpr int U = R::kUnroll;         // packed and fused paths
@@ -1034,6 +1036,184 @@ __global__ __launch_bounds__(kThreads) void persistent_kernel(KCtx cx) {
   }
 }
 
+// Dataflow execution (one launch per piece).  The work queue is the
+// persistent kernel's: per step, worker ids taken in step order from sharded
+// counters, each id running items id, id + G, ...  A work item is either a
+// group of up to kThreads whole edges (chunks under one tile: lanes sweep
+// their vectors as the packed path does) or a run of tiles of one edge.
+// Instead of waiting for the whole previous step, an item waits until the
+// two buffers each of its edges touches have seen every earlier access of the
+// schedule complete: a per-(rank, buffer) counter must reach need * (the
+// count one edge adds): every edge adds its tiles (1 for whole edges) to both
+// of its counters as its items complete, so the unit is the same for every
+// step of a launch, however the steps split their edges into items.  Items wait only on items of earlier steps, which
+// running workgroups hold because ids are taken in step order, so the work
+// always completes whatever the grid size.
+//
+// Ordering across the XCDs' separate L2 caches: each wave waits for its own
+// stores, a workgroup barrier, then the lanes of one wave -- lane t for edge t
+// of the item -- add with agent-scope release (one cache write-back per
+// wave); waiting lanes poll with relaxed agent-scope loads and take an
+// agent-scope acquire before the barrier that lets the other waves load.
+// Every wait is bounded by the wall-clock limit (then the status bit is set
+// and the workgroup stops; the result is undefined).  The last workgroup out
+// zeroes the queue and the buffer counters.
+
+// Ranks of an edge's two counters (DevDep).
+template <class Op>
+__device__ __forceinline__ void dep_ranks(const KCtx& cx, const DevStep& st, int r, int* x1, int* x2) {
+  *x1 = Op::kGather ? r : wrap_add(r, st.d, cx.N);
+  *x2 = Op::kGather ? wrap_add(r, st.d, cx.N) : r;
+}
+
+// Lane t < nedges waits for the counters of edge e0 + t to reach `unit`
+// times their need (unit: the counts one edge adds when it completes, the
+// same for every step of a launch).  Returns false (uniformly) on a timeout.
+template <class Op>
+__device__ bool wait_edges(const KCtx& cx, const DevStep& st, int nedges, int64_t e0, int64_t unit,
+                           QueueShared* q) {
+  if (threadIdx.x == 0) q->flag = 1;
+  __syncthreads();
+  if (threadIdx.x < nedges) {
+    const int64_t e = e0 + threadIdx.x;
+    const int r = (int)(e / st.k), i = (int)(e - (int64_t)r * st.k);
+    const DevDep g = cx.deps[st.entry0 + i];
+    int x1, x2;
+    dep_ranks<Op>(cx, st, r, &x1, &x2);
+    const unsigned t1 = (unsigned)(g.need1 * unit), t2 = (unsigned)(g.need2 * unit);
+    unsigned* c1 = g.e1 >= 0 && t1 ? cx.counters + x1 * cx.counter_stride + g.e1 : nullptr;
+    unsigned* c2 = g.e2 >= 0 && t2 ? cx.counters + x2 * cx.counter_stride + g.e2 : nullptr;
+    if (c1 || c2) {
+      const long long t0 = wall_clock64();
+      for (;;) {
+        const bool ok1 = !c1 || __hip_atomic_load(c1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= t1;
+        const bool ok2 = !c2 || __hip_atomic_load(c2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= t2;
+        if (ok1 && ok2) break;
+        if (wall_clock64() - t0 > cx.timeout_ticks) {
+          __hip_atomic_fetch_or(cx.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          q->flag = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+  }
+  __syncthreads();
+  const int f = q->flag;
+  __syncthreads();
+  return f != 0;
+}
+
+// After the item's stores: lane t < nedges adds `amount` (the tiles of edge
+// e0 + t the item completed) to both of that edge's counters.
+template <class Op>
+__device__ __forceinline__ void signal_edges(const KCtx& cx, const DevStep& st, int nedges, int64_t e0,
+                                             unsigned amount) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x < nedges) {
+    const int64_t e = e0 + threadIdx.x;
+    const int r = (int)(e / st.k), i = (int)(e - (int64_t)r * st.k);
+    const DevDep g = cx.deps[st.entry0 + i];
+    int x1, x2;
+    dep_ranks<Op>(cx, st, r, &x1, &x2);
+    if (g.e1 >= 0)
+      __hip_atomic_fetch_add(cx.counters + x1 * cx.counter_stride + g.e1, amount, __ATOMIC_RELEASE,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    if (g.e2 >= 0)
+      __hip_atomic_fetch_add(cx.counters + x2 * cx.counter_stride + g.e2, amount, __ATOMIC_RELEASE,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// SMALL: every step of the launch is packed (chunks under one tile) and an
+// item is df_edges whole edges; otherwise every step is tiled and an item is
+// df_tiles tiles of one edge.
+template <class Op, bool SMALL>
+__global__ __launch_bounds__(kThreads) void dataflow_kernel(KCtx cx) {
+  __shared__ QueueShared q;
+  bool ok = true;
+  for (int s = 0; s < cx.nsteps && ok;) {
+    const DevStep st = cx.steps[s];
+    const int64_t G = step_ids(cx, s);
+    const int64_t w = take_id(cx, s, G, &q);
+    if (w < 0) {
+      ++s;  // every id of this step is taken
+      continue;
+    }
+    const int64_t edges = (int64_t)cx.N * st.k;
+    for (int64_t item = w; item < st.items; item += G) {
+      if constexpr (SMALL) {
+        const int64_t e0 = item * st.df_edges;
+        const int ne = (int)(edges - e0 < st.df_edges ? edges - e0 : st.df_edges);
+        if (!wait_edges<Op>(cx, st, ne, e0, 1, &q)) {
+          ok = false;
+          break;
+        }
+        constexpr int U = Op::U;
+        const int64_t nv = (int64_t)ne * st.V;
+        for (int64_t base = 0; base < nv; base += (int64_t)kThreads * U) {
+          int rr[U], ii[U];
+          int64_t vv[U];
+#pragma unroll
+          for (int j = 0; j < U; ++j) {
+            const int64_t f = base + j * kThreads + threadIdx.x;
+            vv[j] = -1;
+            rr[j] = 0;
+            ii[j] = 0;
+            if (f < nv) {
+              const int64_t e = e0 + f / st.V;
+              rr[j] = (int)(e / st.k);
+              ii[j] = (int)(e - (int64_t)rr[j] * st.k);
+              vv[j] = f - (f / st.V) * st.V;
+            }
+          }
+          Op::template batch<false>(cx, st, rr, ii, vv);
+        }
+        signal_edges<Op>(cx, st, ne, e0, 1u);
+      } else {
+        const int64_t per_edge = (st.tiles_per_edge + st.df_tiles - 1) / st.df_tiles;
+        const int64_t e = item / per_edge;
+        const int64_t t0 = (item - e * per_edge) * st.df_tiles;
+        const int64_t t1 = t0 + st.df_tiles < st.tiles_per_edge ? t0 + st.df_tiles : st.tiles_per_edge;
+        if (!wait_edges<Op>(cx, st, 1, e, st.tiles_per_edge, &q)) {
+          ok = false;
+          break;
+        }
+        for (int64_t t = t0; t < t1; ++t) Op::run(cx, st, e * st.tiles_per_edge + t);
+        signal_edges<Op>(cx, st, 1, e, (unsigned)(t1 - t0));
+      }
+    }
+  }
+  // Leave the queue and the counters at zero: the last workgroup out (every
+  // other one has finished all of its work by then) resets them.
+  __syncthreads();
+  if (threadIdx.x == 0)
+    q.flag = (__hip_atomic_fetch_add(&cx.queue[1], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u == gridDim.x);
+  __syncthreads();
+  if (q.flag) {
+    const int64_t n = (2 * (int64_t)kShards + 1) * cx.nsteps;
+    for (int64_t k = threadIdx.x; k < n; k += blockDim.x)
+      __hip_atomic_store(queue_line(cx, k), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t nc = (int64_t)cx.N * cx.counter_stride;
+    for (int64_t k = threadIdx.x; k < nc; k += blockDim.x)
+      __hip_atomic_store(cx.counters + k, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_store(&cx.queue[1], 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+template <class Op>
+hipError_t launch_dataflow_t(const KCtx& cx, bool small, int grid, hipStream_t stream) {
+  if (small)
+    hipLaunchKernelGGL((dataflow_kernel<Op, true>), dim3(grid), dim3(kThreads), 0, stream, cx);
+  else
+    hipLaunchKernelGGL((dataflow_kernel<Op, false>), dim3(grid), dim3(kThreads), 0, stream, cx);
+  return hipGetLastError();
+}
+
 template <class Op>
 hipError_t launch_step_t(const KCtx& cx, const DevStep& st, int64_t grain, hipStream_t stream) {
   const int64_t items = st.items;
@@ -1180,6 +1360,12 @@ hipError_t launch_persistent(Variant v, bool streaming, const KCtx& cx, int grid
 #define PAT_PERS(OP) launch_persistent_t<PAT_UNPAREN OP>(cx, grid, stream)
   PAT_DISPATCH(v, streaming, PAT_PERS)
 #undef PAT_PERS
+}
+
+hipError_t launch_dataflow(Variant v, bool streaming, const KCtx& cx, bool small, int grid, hipStream_t stream) {
+#define PAT_DF(OP) launch_dataflow_t<PAT_UNPAREN OP>(cx, small, grid, stream)
+  PAT_DISPATCH(v, streaming, PAT_DF)
+#undef PAT_DF
 }
 
 hipError_t persistent_capacity(Variant v, bool streaming, int* blocks) {

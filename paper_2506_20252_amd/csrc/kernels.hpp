@@ -38,6 +38,10 @@ struct KCtx {
   unsigned* status;           // bit 0: a persistent kernel's wait timed out
   uint64_t* stamps;           // fused launches, measurement only (null: off): per workgroup, the device
                               // wall clock before its first step and after each step, (s1 - s0 + 1) apiece
+  const DevDep* deps;         // dataflow execution: per entry of the step table, the counters it waits on
+  unsigned* counters;         // dataflow execution: [N][counter_stride] completed tiles per buffer (zero
+                              // between launches)
+  int64_t counter_stride;     // slot entries per rank + 1 (the own chunk's accumulator)
 };
 
 // Words of the persistent kernel's counter area for `nsteps` launch-level steps.
@@ -94,6 +98,13 @@ hipError_t launch_tree(Variant v, bool streaming, const KCtx& cx, const TreeRang
 // worker ids from device counters in step order.  Any grid size is safe (a
 // workgroup only waits on work that running workgroups already hold).
 hipError_t launch_persistent(Variant v, bool streaming, const KCtx& cx, int grid, hipStream_t stream);
+// Dataflow execution: one launch per piece (cx.steps: that piece's steps,
+// cx.nsteps of them), workgroups taking per-step worker ids like the
+// persistent kernel, every work item waiting only for the counters of the
+// buffers its edges touch.  small: every step packs whole edges into items
+// (DevStep::df_edges, chunks under one tile); else items are DevStep::df_tiles
+// tiles of one edge.  Any grid size is safe.
+hipError_t launch_dataflow(Variant v, bool streaming, const KCtx& cx, bool small, int grid, hipStream_t stream);
 // Workgroups of the persistent kernel that fit on the current device at once.
 hipError_t persistent_capacity(Variant v, bool streaming, int* blocks);
 

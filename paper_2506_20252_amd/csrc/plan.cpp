@@ -214,6 +214,35 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, in
   return true;
 }
 
+bool dataflow_deps(const PlanDesc& d, std::vector<DevDep>* deps) {
+  const int root = d.slots.entries;  // counter index of the own chunk's accumulator
+  std::vector<int32_t> done(size_t(root) + 1, 0);  // accesses completed before the current step
+  deps->assign(d.entries.size(), DevDep{-1, 0, -1, 0});
+  for (const auto& st : d.exec) {
+    std::vector<int32_t> now(done);
+    for (int j = 0; j < st.k; ++j) {
+      const DevEntry& e = d.entries[st.first + j];
+      DevDep& g = (*deps)[st.first + j];
+      if (d.coll == 0) {
+        g.e1 = e.a >= 0 ? e.a : -1;  // the sender's slot (-1: its own send buffer)
+        g.e2 = e.b >= 0 ? e.b : -1;  // the receiver's slot (-1: receive buffer only)
+      } else {
+        g.e1 = e.a >= 0 ? e.a : -1;     // the child's accumulator (-1: a leaf's raw input)
+        g.e2 = e.c >= 0 ? e.c : root;   // the receiver's accumulator or its own chunk's
+      }
+      for (int32_t* ep : {&g.e1, &g.e2}) {
+        if (*ep < 0) continue;
+        if (now[*ep] != done[*ep]) return false;  // a second access in one step
+        ++now[*ep];
+      }
+      if (g.e1 >= 0) g.need1 = done[g.e1];
+      if (g.e2 >= 0) g.need2 = done[g.e2];
+    }
+    done.swap(now);
+  }
+  return true;
+}
+
 double step_bytes(const PlanDesc& d, int s, int64_t elems) {
   if (d.N <= 1 || elems <= 0 || s < 0 || s >= (int)d.exec.size()) return 0.0;
   const double ei = d.esize_in, es = d.esize_slot;

@@ -85,6 +85,14 @@ struct PlanDesc {
 // Budget in bytes per slot.  Returns false for unsupported arguments.
 bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out);
 
+// Dependencies of every entry of d.entries for dataflow execution (one piece
+// in execution order): for each of the two buffers an edge touches, the
+// number of accesses to that buffer in earlier steps (see DevDep).  The
+// schedule is the same for every rank up to a shift, so these counts hold at
+// every rank.  Returns false if two edges of one step would touch one buffer
+// (the schedules never do).
+bool dataflow_deps(const PlanDesc& d, std::vector<DevDep>* deps);
+
 // Algorithmic memory bytes of one operation (read + written by the steps):
 // all-gather: per chunk-edge, read C, write C to the receiver's buffer, write
 // C again to its slot when it forwards (plus each rank's own chunk, C);

@@ -41,7 +41,9 @@ PAT_REDUCESCATTER = 1
 PAT_EXEC_PERSISTENT = 0
 PAT_EXEC_GRAPH = 1
 PAT_EXEC_STREAM = 2
-MODES = {"persistent": PAT_EXEC_PERSISTENT, "graph": PAT_EXEC_GRAPH, "stream": PAT_EXEC_STREAM}
+PAT_EXEC_DATAFLOW = 3
+MODES = {"persistent": PAT_EXEC_PERSISTENT, "graph": PAT_EXEC_GRAPH, "stream": PAT_EXEC_STREAM,
+         "dataflow": PAT_EXEC_DATAFLOW}
 
 PAT_LINEAR_FAR_FIRST = 0
 PAT_LINEAR_CLOSE_FIRST = 1

@@ -2,15 +2,107 @@
 // tests/test_host_sanitizers.py.  For many (ranks, count, budget, order) it
 // builds plans and checks their tables: every tree edge once per piece, slot
 // indices inside the slot map, each non-root receiver starting from its own
-// input exactly once.
+// input exactly once.  For N <= 64 it also runs the dataflow dependency table
+// (dataflow_deps) symbolically: edges execute in orders that respect nothing
+// but their counters (shuffled, and latest step first), and every transfer
+// must find what the schedule promises -- the chunk a sender forwards, the
+// partial sums a receiver adds -- with no edge left unable to run.
+#include <algorithm>
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
+#include <random>
 #include <vector>
 
 #include "plan.hpp"
 
+namespace {
+
+struct Edge {
+  int step, r, j;
+};
+
+// Returns an error message, or nullptr.
+const char* simulate_dataflow(const pat::PlanDesc& d, uint32_t seed, bool latest_first) {
+  const int N = d.N, E = d.slots.entries, root = E;
+  std::vector<pat::DevDep> deps;
+  if (!pat::dataflow_deps(d, &deps)) return "dataflow_deps refused the plan";
+  std::vector<uint32_t> ctr(size_t(N) * (E + 1), 0);
+  // Buffer contents: all-gather slots hold a chunk id (+1, 0 empty); reduce-
+  // scatter accumulators hold (chunk id, mask of contributing ranks).
+  std::vector<int> ag_slot(size_t(N) * E, 0);
+  std::vector<uint64_t> ag_have(N, 0);
+  std::vector<int> rs_chunk(size_t(N) * (E + 1), -1);
+  std::vector<uint64_t> rs_mask(size_t(N) * (E + 1), 0);
+  for (int r = 0; r < N; ++r) ag_have[r] = uint64_t(1) << r;
+  std::vector<Edge> pending;
+  for (int s = 0; s < (int)d.exec.size(); ++s)
+    for (int r = 0; r < N; ++r)
+      for (int i = 0; i < d.exec[s].k; ++i) pending.push_back({s, r, d.exec[s].first + i});
+  std::mt19937 rng(seed);
+  auto at = [&](int x, int e) { return size_t(x) * (E + 1) + e; };
+  while (!pending.empty()) {
+    std::shuffle(pending.begin(), pending.end(), rng);
+    if (latest_first)
+      std::stable_sort(pending.begin(), pending.end(), [](const Edge& a, const Edge& b) { return a.step > b.step; });
+    std::vector<Edge> left;
+    bool progress = false;
+    for (const Edge& ed : pending) {
+      const pat::StepSpec& st = d.exec[ed.step];
+      const pat::DevEntry& en = d.entries[ed.j];
+      const pat::DevDep& g = deps[ed.j];
+      const int r = ed.r, peer = (r + st.d) % N;
+      const int x1 = d.coll == 0 ? r : peer, x2 = d.coll == 0 ? peer : r;
+      if ((g.e1 >= 0 && ctr[at(x1, g.e1)] < (uint32_t)g.need1) || (g.e2 >= 0 && ctr[at(x2, g.e2)] < (uint32_t)g.need2)) {
+        left.push_back(ed);
+        continue;
+      }
+      const int c = ((r - en.p) % N + N) % N;  // the tree (chunk) of this edge
+      if (d.coll == 0) {
+        if (en.p != 0 && ag_slot[size_t(r) * E + en.a] != c + 1) return "all-gather: sender's slot does not hold the chunk";
+        if (ag_have[peer] >> c & 1) return "all-gather: chunk received twice";
+        ag_have[peer] |= uint64_t(1) << c;
+        if (en.b >= 0) ag_slot[size_t(peer) * E + en.b] = c + 1;
+      } else {
+        uint64_t child;
+        if (en.a < 0) {
+          child = uint64_t(1) << peer;
+        } else {
+          if (rs_chunk[at(peer, en.a)] != c) return "reduce-scatter: child's accumulator holds another chunk";
+          child = rs_mask[at(peer, en.a)];
+        }
+        uint64_t own;
+        const int ob = en.b >= 0 ? en.b : en.b == pat::kRoot ? root : -1;
+        if (ob < 0) {
+          own = uint64_t(1) << r;
+        } else {
+          if (rs_chunk[at(r, ob)] != c) return "reduce-scatter: own accumulator holds another chunk";
+          own = rs_mask[at(r, ob)];
+        }
+        if (own & child) return "reduce-scatter: a contribution added twice";
+        const int oc = en.c >= 0 ? en.c : root;
+        rs_chunk[at(r, oc)] = c;
+        rs_mask[at(r, oc)] = own | child;
+      }
+      if (g.e1 >= 0) ++ctr[at(x1, g.e1)];
+      if (g.e2 >= 0) ++ctr[at(x2, g.e2)];
+      progress = true;
+    }
+    if (!progress) return "dataflow deadlock: no pending edge can run";
+    pending.swap(left);
+  }
+  const uint64_t all = N == 64 ? ~uint64_t(0) : (uint64_t(1) << N) - 1;
+  for (int r = 0; r < N; ++r) {
+    if (d.coll == 0 && ag_have[r] != all) return "all-gather: a rank misses a chunk";
+    if (d.coll == 1 && (rs_chunk[at(r, root)] != r || rs_mask[at(r, root)] != all)) return "reduce-scatter: wrong sum";
+  }
+  return nullptr;
+}
+
+}  // namespace
+
 int main() {
-  long plans = 0;
+  long plans = 0, dataflow_runs = 0;
   const size_t budgets[] = {16, 4096, 65536, size_t(8) << 20};
   for (int N = 1; N <= 300; ++N) {
     for (int order = 0; order < 2; ++order) {
@@ -46,11 +138,20 @@ int main() {
                   return 1;
                 }
               }
+            if (N <= 64 && count == 17) {
+              for (int mode = 0; mode < 2; ++mode) {
+                if (const char* err = simulate_dataflow(d, uint32_t(N * 7919 + order * 31 + coll), mode == 1)) {
+                  std::fprintf(stderr, "N=%d coll=%d budget=%zu order=%d: %s\n", N, coll, budget, order, err);
+                  return 1;
+                }
+                ++dataflow_runs;
+              }
+            }
           }
         }
       }
     }
   }
-  std::printf("plans checked: %ld\n", plans);
+  std::printf("plans checked: %ld, dataflow simulations: %ld\n", plans, dataflow_runs);
   return 0;
 }

@@ -208,14 +208,14 @@ def test_device_fill_matches_host_twin(dist):
 # The five workloads
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 def test_workload1_rs_int32_n6(mode):
     n, count, seed = 6, 1024, 0x5041541
     got = run_rs(n, count, "int32", seed, mode=mode)
     check_rs(got, host_rs_inputs(n, count, "int32_pm2p20", seed), "int32", 0)
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 def test_workload2_ag_bf16_n24(mode):
     n, count, seed = 24, 32768, 0x5041542
     st, info = pat.pat_plan_info(pat.PAT_ALLGATHER, n, count, "bfloat16")
@@ -226,13 +226,13 @@ def test_workload2_ag_bf16_n24(mode):
 
 def test_workload3_rs_f32_n64_every_element():
     """Workload 3 at its full size (N = 64, 1 MiB output chunks): every output
-    element of every destination, in all three execution modes."""
+    element of every destination, in all four execution modes."""
     n, count, seed = 64, 262144, 0x5041543
-    outs = run_rs_modes(n, count, "float32", seed, ["stream", "graph", "persistent"])
+    outs = run_rs_modes(n, count, "float32", seed, ["stream", "graph", "persistent", "dataflow"])
     compare_rs_full(outs, n, count, "float32", "f32_normal", seed)
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 def test_workload4_small_chunks_n1000(mode):
     """The small-size regime (N = 1000, 64 fp32 per chunk) as the benchmark
     runs it (AUTO fusion: 10 steps in 3 launches in stream and graph modes):
@@ -252,10 +252,10 @@ def test_workload4_small_chunks_n1000(mode):
 def test_workload5_rs_bf16_n128_every_element():
     """Workload 5 at its full size (N = 128, bf16 inputs, 4 MiB output chunks,
     64 GiB of send buffers): every one of the 128 x 2,097,152 outputs, in
-    stream and graph modes, bit-exact against the PAT order and within 1e-2 of
-    the fp64 sum."""
+    stream, graph and dataflow modes, bit-exact against the PAT order and
+    within 1e-2 of the fp64 sum."""
     n, count, seed = 128, 2 * MIB, 0x5041545
-    outs = run_rs_modes(n, count, "bfloat16", seed, ["stream", "graph"])
+    outs = run_rs_modes(n, count, "bfloat16", seed, ["stream", "graph", "dataflow"])
     pat.check(pat.pat_finalize())
     torch.cuda.empty_cache()
     compare_rs_full(outs, n, count, "bfloat16", "bf16_normal", seed)
@@ -370,7 +370,7 @@ def test_sweep_default_budget(n, dtype, count, mode):
 
 @pytest.mark.parametrize("n", [5, 8, 13, 33])
 @pytest.mark.parametrize("budget", [4096, 16384, 65536])
-@pytest.mark.parametrize("mode", ["persistent", "graph", "stream"])
+@pytest.mark.parametrize("mode", ["persistent", "graph", "stream", "dataflow"])
 def test_sweep_budgets_and_modes(n, budget, mode):
     count = 4104  # float32: 16416-byte chunks, so 4096 B forces pieces and a ragged last piece
     pat.check(pat.pat_set_buffer_bytes(budget))
@@ -387,7 +387,7 @@ def test_sweep_budgets_and_modes(n, budget, mode):
 
 
 @pytest.mark.parametrize("count", [1000, 1001, 1004])  # aligned; partial last vectors; bf16 RS 4-element vectors
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 @pytest.mark.parametrize("n", [1, 6, 9])
 def test_in_place(n, dtype, mode, count):
@@ -465,7 +465,32 @@ def test_persistent_barrier_timeout_is_reported_and_recovers():
              oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+def test_dataflow_wait_timeout_is_reported_and_recovers():
+    """Failure handling forced from the host: a 1 us limit on the dataflow
+    kernel's bounded waits for the buffers of earlier steps (1 MiB chunks:
+    no step completes that fast).  Every workgroup still exits; the timeout
+    is reported once, and the next operation on the same plan is correct."""
+    n, count, seed = 64, 262144, 0x78
+    pat.check(pat.pat_set_barrier_timeout_us(1))
+    try:
+        dev = torch.device("cuda:0")
+        send = torch.empty((n, n * count), dtype=torch.float32, device=dev)
+        fill_ranks(send, "f32_normal", seed)
+        recv = torch.empty((n, count), dtype=torch.float32, device=dev)
+        pat.check(pat.pat_set_exec_mode("dataflow"))
+        stream = torch.cuda.current_stream()
+        log("[gpu] dataflow reduce-scatter with a 1 us wait limit")
+        pat.check(pat.pat_reducescatter(list(send), list(recv), count, "float32", pat.PAT_SUM, n, stream))
+        assert pat.pat_check_device_status(stream) == pat.PAT_ERR_TIMEOUT
+        assert pat.pat_check_device_status(stream) == pat.PAT_OK
+        del send, recv
+    finally:
+        pat.check(pat.pat_set_barrier_timeout_us(0))
+    outs = run_rs_modes(n, count, "float32", seed, ["dataflow"])
+    compare_rs_full(outs, n, count, "float32", "f32_normal", seed)
+
+
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 def test_back_to_back_calls_with_new_buffers_no_host_sync(mode):
     """Three operations on one plan, each with its own buffers, queued without
     any host synchronisation: the pointer tables are re-staged each call while
@@ -807,7 +832,7 @@ def _random_cases(k=100, seed=2026):
         dtype = str(rng.choice(["int32", "float32", "bfloat16"]))
         count = int(rng.choice([1, 3, 8, 33, 250, 1000, 2052]))
         budget = int(rng.choice([0, 64, 512, 4096, 65536]))  # 0: default; small budgets force pieces
-        mode = str(rng.choice(["stream", "graph", "persistent"]))
+        mode = str(rng.choice(["stream", "graph", "persistent", "dataflow"]))
         fusion = str(rng.choice(["auto", "on", "off"]))
         order = str(rng.choice(["far", "close"]))
         coll = str(rng.choice(["ag", "rs"]))
@@ -837,7 +862,7 @@ def test_random_configurations(case):
         pat.check(pat.pat_set_linear_order("far"))
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 def test_caller_created_stream(mode):
     """The collectives run on the stream they are given, not only on the
     default one."""
@@ -972,7 +997,7 @@ def _rows(flat, n, length, skew):
     return [flat[skew + r * length: skew + (r + 1) * length] for r in range(n)]
 
 
-@pytest.mark.parametrize("mode", ["stream", "graph", "persistent"])
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 def test_relaxed_vectors_at_element_offsets(dtype, mode):
     """Buffers one element past a 16-byte boundary, and counts just under,
@@ -1038,7 +1063,7 @@ def _skewed_cases(k=60, seed=2027):
         dtype = str(rng.choice(["int32", "float32", "bfloat16"]))
         count = int(rng.choice([4, 7, 12, 64, 333, 1024, 2051, 4099]))
         budget = int(rng.choice([0, 100, 1000, 4096]))  # small budgets: pieces, each with its partial vector
-        mode = str(rng.choice(["stream", "graph", "persistent"]))
+        mode = str(rng.choice(["stream", "graph", "persistent", "dataflow"]))
         fusion = str(rng.choice(["auto", "on", "off"]))
         order = str(rng.choice(["far", "close"]))
         coll = str(rng.choice(["ag", "rs"]))
