@@ -340,11 +340,13 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
     return out
 
 
-def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
+def budget_sweep(wid, reps, max_slot_bytes=32 << 30, aggregation="pow2"):
     """Time one workload at every aggregation level: the budget is set to the
     bytes of the largest step at T = 1, 2, 4, ... up to full aggregation, so
     the plan goes from one linear tree (N - 1 steps) to ceil(log2 N) steps,
-    stopping early once the slots of all ranks would exceed max_slot_bytes."""
+    stopping early once the slots of all ranks would exceed max_slot_bytes.
+    With aggregation "budget" the budget also takes 3, 5, 6 and 7 chunks
+    (K chunks per step, the list schedule where it is shorter)."""
     import torch
 
     import synth
@@ -366,13 +368,19 @@ def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
         synth.fill(send[x], dist, seed, x)
     S, R = pat.pointer_array(list(send)), pat.pointer_array(list(recv))
     slot_elem = 4 if (coll == "rs" or dtype != "bfloat16") else (2 if dtype == "bfloat16" else 4)
+    pat.check(pat.pat_set_aggregation(aggregation))
     rows = []
+    Ks = [1, 2, 3, 4, 5, 6, 7, 8] if aggregation == "budget" else []
     T = 1
     while True:
+        if Ks:
+            T = Ks.pop(0)
         budget = T * count * slot_elem
         pat.check(pat.pat_set_buffer_bytes(budget))
         st, info = pat.pat_plan_info(code, n, count, dtype)
-        if info["T"] < T or info["slot_bytes_total"] > max_slot_bytes:
+        if (info["T"] < T and not info["list_schedule"]) or info["slot_bytes_total"] > max_slot_bytes:
+            if Ks:
+                continue
             break
 
         def op():
@@ -391,18 +399,22 @@ def budget_sweep(wid, reps, max_slot_bytes=32 << 30):
         torch.cuda.synchronize()
         pat.check(pat.pat_check_device_status(stream))
         sec = e0.elapsed_time(e1) / 1e3 / reps
-        rows.append({"budget_bytes": budget, "T": info["T"], "steps": info["steps"],
+        rows.append({"budget_bytes": budget, "T": info["T"], "list_schedule": bool(info["list_schedule"]),
+                     "steps": info["steps"],
                      "launches": info["launches_per_op"],
                      "slot_bytes_per_rank": info["slot_bytes_per_rank"], "us": round(sec * 1e6, 2),
                      "bus_gbps": round(n * info["bus_bytes_per_rank"] / sec / 1e9, 2),
                      "hbm_frac_alg": round(info["alg_bytes"] / sec / 1e9 / HBM_PEAK_GBPS, 4)})
         pat.check(pat.pat_finalize())
+        if Ks:
+            continue
         if info["T"] * 2 > (1 << max(info["L"] - 1, 0)):
             break
-        T *= 2
+        T *= 2  # after the listed K (1 .. 8 with "budget"), powers of two
     pat.check(pat.pat_set_buffer_bytes(0))
+    pat.check(pat.pat_set_aggregation("pow2"))
     print(json.dumps({"metric": "PAT budget sweep (steps and time per aggregation level)", "workload": desc,
-                      "exec_mode": ["persistent", "graph", "stream", "dataflow"][pat.pat_get_exec_mode()],
+                      "aggregation": aggregation, "exec_mode": ["persistent", "graph", "stream", "dataflow"][pat.pat_get_exec_mode()],
                       "nranks": n, "log2_n": round(math.log2(n), 3), "rows": rows}), flush=True)
 
 
@@ -682,6 +694,8 @@ def main():
     ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-ceiling probes")
     ap.add_argument("--budget-sweep", action="store_true",
                     help="instead: time the workload at every aggregation level (T = 1 .. full)")
+    ap.add_argument("--aggregation", default="pow2", choices=["pow2", "budget"],
+                    help="with --budget-sweep: power-of-two sub-trees, or any chunks per step (list schedule)")
     ap.add_argument("--step-clock", action="store_true",
                     help="instead: per-step device clock of the workload's fused launch (PAT_STEP_CLOCK=1)")
     ap.add_argument("--size-sweep", action="store_true",
@@ -700,7 +714,7 @@ def main():
     from paper_2506_20252_amd import pat as _pat
     _pat.check(_pat.pat_set_exec_mode(args.mode))  # the sweeps run in the chosen mode too
     if args.budget_sweep:
-        budget_sweep(args.workload, args.steps)
+        budget_sweep(args.workload, args.steps, aggregation=args.aggregation)
         return
     if args.size_sweep:
         size_sweep()

@@ -191,6 +191,24 @@ typedef enum { PAT_LINEAR_FAR_FIRST = 0, PAT_LINEAR_CLOSE_FIRST = 1 } pat_linear
 pat_status_t pat_set_linear_order(int order);
 int pat_get_linear_order(void);
 
+/*
+ * Aggregation rule (section "The PAT algorithm": as many parallel sub-trees
+ * as the buffer permits).  PAT_AGGREGATION_POW2, the default, takes T = 2^t
+ * sub-trees, the largest power of two whose steps fit the budget, as in the
+ * paper's examples.  PAT_AGGREGATION_BUDGET lets a step carry any number
+ * K = floor(B / chunk bytes) of chunks: where K is not a power of two (or the
+ * rank count is not), a list schedule -- still one peer per step, each node
+ * forwarding farthest child first, at most K chunks per slot -- may need
+ * fewer steps, and replaces the power-of-two schedule then (never with
+ * pieces).  The reduce-scatter's summation order is the same either way.  A
+ * list schedule runs without fused launches (its slot entries pass between
+ * trees).  Default: PAT_AGGREGATION_POW2, or the PAT_AGGREGATION environment
+ * variable (pow2 | budget).  Affects plans created afterwards.
+ */
+typedef enum { PAT_AGGREGATION_POW2 = 0, PAT_AGGREGATION_BUDGET = 1 } pat_aggregation_t;
+pat_status_t pat_set_aggregation(int mode);
+int pat_get_aggregation(void);
+
 /* Execution mode (pat_exec_mode_t).  Default: PAT_EXEC_STREAM, or the
  * PAT_EXEC_MODE environment variable (persistent | graph | stream | dataflow). */
 pat_status_t pat_set_exec_mode(int mode);
@@ -253,6 +271,7 @@ typedef struct {
   int streaming;              /* 1: nontemporal loads and stores (operations of >= 1e9 algorithmic bytes) */
   int xcd_run;                /* step kernels: each XCD takes runs of this many consecutive work items
                                  (0: a contiguous eighth of each step; all-gather 0, reduce-scatter 32) */
+  int list_schedule;          /* 1: the list schedule of PAT_AGGREGATION_BUDGET (T = chunks per step) */
 } pat_plan_info_t;
 
 pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_dtype_t dtype,

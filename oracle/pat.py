@@ -201,7 +201,7 @@ def children(nranks: int, p: int, reach: int) -> int:
     return n
 
 
-def allgather(inputs: np.ndarray, t: int, order: str = "far"):
+def allgather(inputs: np.ndarray, t: int, order: str = "far", steps=None):
     """Execute the all-gather steps on per-rank data.
 
     inputs: (N, m) -- rank x's send buffer.  Returns (recv, stats): recv is
@@ -213,6 +213,10 @@ def allgather(inputs: np.ndarray, t: int, order: str = "far"):
     forward.  A chunk that will not be forwarded goes only to the receive
     buffer.  Every transfer is checked: the sender holds the chunk, the
     receiver never gets a chunk twice.
+
+    `steps`, if given, replaces schedule(N, t, order): any list of (d, P) in
+    the same form (e.g. another schedule under test), executed and checked the
+    same way.
     """
     inputs = np.asarray(inputs)
     N = inputs.shape[0]
@@ -223,7 +227,7 @@ def allgather(inputs: np.ndarray, t: int, order: str = "far"):
         have[r, r] = True
     buf = [dict() for _ in range(N)]  # rank -> {(d, chunk): [data, forwards left]}
     peak = {}  # d -> most chunks any rank held for dimension d at once
-    steps = schedule(N, t, order)
+    steps = schedule(N, t, order) if steps is None else steps
     for d, P in steps:
         messages = []
         for r in range(N):
@@ -287,7 +291,7 @@ def _add(a, b, dtype):
     return (a + b).astype(np.float32)  # float32 + float32, one rounding
 
 
-def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far"):
+def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far", steps=None):
     """Execute the reduce-scatter steps (reversed trees) on per-rank data.
 
     inputs: (N, N, m) -- inputs[x][c] is rank x's contribution to chunk c.
@@ -303,6 +307,9 @@ def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far"):
     chunk (p == 0), to its receive buffer.  Adds are single float32 roundings
     (int32 wraps); bfloat16 partials are carried in float32 and the receive
     buffer is rounded to bfloat16 once, after the last receive.
+
+    `steps`, if given, replaces schedule(N, t, order) as the all-gather steps
+    whose reversal is executed (checked the same way).
     """
     inputs = np.asarray(inputs)
     N = inputs.shape[0]
@@ -311,7 +318,7 @@ def reducescatter(inputs: np.ndarray, t: int, dtype: str, order: str = "far"):
     root = [None] * N   # rank -> its own chunk's running sum
     acc = [dict() for _ in range(N)]  # rank -> {(d, chunk): partial}
     peak = {}
-    steps = list(reversed(schedule(N, t, order)))
+    steps = list(reversed(schedule(N, t, order) if steps is None else steps))
     for d, P in steps:
         arriving = []
         for r in range(N):

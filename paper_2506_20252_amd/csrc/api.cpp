@@ -29,6 +29,7 @@ int g_mode = -1;         // -1: environment / default
 uint32_t g_timeout_us = 0;  // 0: default
 int g_order = -1;           // -1: environment / default (far-first)
 int g_fusion = -1;          // -1: environment / default (auto)
+int g_aggregation = -1;     // -1: environment / default (power-of-two sub-trees)
 std::atomic<int> g_last_hip{0};
 
 size_t budget_now() {
@@ -55,6 +56,13 @@ int order_now() {
   if (const char* e = std::getenv("PAT_LINEAR_ORDER"))
     if (!std::strcmp(e, "close")) return pat::kCloseFirst;
   return pat::kFarFirst;
+}
+
+int aggregation_now() {
+  if (g_aggregation >= 0) return g_aggregation;
+  if (const char* e = std::getenv("PAT_AGGREGATION"))
+    if (!std::strcmp(e, "budget")) return PAT_AGGREGATION_BUDGET;
+  return PAT_AGGREGATION_POW2;
 }
 
 int fusion_now() {
@@ -115,7 +123,7 @@ int64_t tree_fuse_bytes() { return env_or("PAT_TREE_FUSE_BYTES", int64_t(128) <<
 void fused_range(const pat::PlanDesc& d, int64_t V, int fusion, int* s0, int* s1, int64_t* tile_vecs) {
   *s0 = *s1 = 0;
   *tile_vecs = std::max<int64_t>(1, std::min<int64_t>(V, tree_tile_vecs(d.N, V)));
-  if (fusion == PAT_FUSION_OFF || d.pieces != 1) return;
+  if (fusion == PAT_FUSION_OFF || d.pieces != 1 || d.sched.list) return;  // list schedules share slots across trees
   const int ns = (int)d.exec.size(), t = d.sched.t;
   const bool whole = d.sched.M <= 4;
   int lo = whole || d.coll == 0 ? 0 : ns - t, hi = whole || d.coll == 1 ? ns : t;
@@ -273,7 +281,8 @@ struct Plan {
   }
 };
 
-using PlanKey = std::tuple<int, int, int64_t, int, size_t, int, int>;  // coll, N, count, dtype, budget, order, device
+// coll, N, count, dtype, budget, linear order, device, aggregation
+using PlanKey = std::tuple<int, int, int64_t, int, size_t, int, int, int>;
 std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
 uint64_t g_tick = 0;
 
@@ -377,9 +386,9 @@ pat::Variant variant_for(int coll, pat_dtype_t dt, int path) {
 int aligned_path(const bool (&has)[3]) { return has[1] ? 1 : has[2] ? 2 : 0; }
 
 // Schedule tables and slot layout of a plan (host memory only).
-pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order,
+pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int agg,
                             HostPlan* h) {
-  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &h->desc)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &h->desc, agg)) return PAT_ERR_INVALID_ARGUMENT;
   const pat::PlanDesc& d = h->desc;
   for (int path = 0; path < 3; ++path) {
     const pat::Variant v = variant_for(coll, dt, path);
@@ -397,10 +406,10 @@ pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size
   return PAT_OK;
 }
 
-pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int device,
-                         Plan** out) {
+pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int agg,
+                         int device, Plan** out) {
   auto p = std::make_unique<Plan>();
-  const pat_status_t hs = make_host_plan(coll, N, count, dt, budget, order, &p->h);
+  const pat_status_t hs = make_host_plan(coll, N, count, dt, budget, order, agg, &p->h);
   if (hs != PAT_OK) return hs;
   const HostPlan& h = p->h;
   const pat::PlanDesc& d = h.desc;
@@ -469,7 +478,7 @@ pat_status_t create_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t 
     }
   }
   *out = p.get();
-  g_plans[PlanKey(coll, N, count, (int)dt, budget, order, device)] = std::move(p);
+  g_plans[PlanKey(coll, N, count, (int)dt, budget, order, device, agg)] = std::move(p);
   return PAT_OK;
 }
 
@@ -750,12 +759,13 @@ pat_status_t run(int coll, const void* const* send, void* const* recv, size_t co
   HIP_TRY(hipGetDevice(&device));
   const size_t budget = budget_now();
   const int order = order_now();
+  const int agg = aggregation_now();
   Plan* plan = nullptr;
-  auto it = g_plans.find(PlanKey(coll, N, (int64_t)count, (int)dt, budget, order, device));
+  auto it = g_plans.find(PlanKey(coll, N, (int64_t)count, (int)dt, budget, order, device, agg));
   if (it != g_plans.end()) {
     plan = it->second.get();
   } else {
-    const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, order, device, &plan);
+    const pat_status_t s = create_plan(coll, N, (int64_t)count, dt, budget, order, agg, device, &plan);
     if (s != PAT_OK) return s;
   }
   const HostPlan& h = plan->h;
@@ -952,7 +962,7 @@ pat_status_t run_noalloc(int coll, const void* const* send, void* const* recv, s
   char* base = nullptr;
   HIP_TRY(pat::scratch_base(device, &base));  // this device's array (looked up once per device)
   ScratchState& ss = g_scratch[device];
-  const PlanKey key(coll, N, (int64_t)count, (int)dt, budget_now(), order_now(), device);
+  const PlanKey key(coll, N, (int64_t)count, (int)dt, budget_now(), order_now(), device, aggregation_now());
   if (!ss.have_plan || ss.key != key) {
     // A new plan: its tables must be uploaded before use.
     ss.have_plan = false;
@@ -960,7 +970,8 @@ pat_status_t run_noalloc(int coll, const void* const* send, void* const* recv, s
     ss.send.clear();
     ss.recv.clear();
     ss.plan = HostPlan();
-    const pat_status_t s = make_host_plan(coll, N, (int64_t)count, dt, std::get<4>(key), std::get<5>(key), &ss.plan);
+    const pat_status_t s =
+        make_host_plan(coll, N, (int64_t)count, dt, std::get<4>(key), std::get<5>(key), std::get<7>(key), &ss.plan);
     if (s != PAT_OK) return s;
     if (scratch_layout(ss.plan, N, &ss) > pat::scratch_bytes()) return PAT_ERR_TOO_LARGE;
     ss.key = key;
@@ -1001,13 +1012,14 @@ pat_status_t describe(int coll, int N, size_t count, pat_dtype_t dt, pat::PlanDe
   if (dt != PAT_INT32 && dt != PAT_FLOAT32 && dt != PAT_BFLOAT16) return PAT_ERR_UNSUPPORTED;
   if (count > (size_t(1) << 40)) return PAT_ERR_INVALID_ARGUMENT;
   size_t budget;
-  int order;
+  int order, agg;
   {
     std::lock_guard<std::mutex> lock(g_mu);
     budget = budget_now();
     order = order_now();
+    agg = aggregation_now();
   }
-  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, order, d)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, order, d, agg)) return PAT_ERR_INVALID_ARGUMENT;
   return PAT_OK;
 }
 
@@ -1065,6 +1077,18 @@ pat_status_t pat_set_top_fusion(int mode) {
 int pat_get_top_fusion(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   return fusion_now();
+}
+
+pat_status_t pat_set_aggregation(int mode) {
+  if (mode != PAT_AGGREGATION_POW2 && mode != PAT_AGGREGATION_BUDGET) return PAT_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(g_mu);
+  g_aggregation = mode;
+  return PAT_OK;
+}
+
+int pat_get_aggregation(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  return aggregation_now();
 }
 
 pat_status_t pat_set_linear_order(int order) {
@@ -1133,6 +1157,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   }
   info.streaming = streaming_for(d.alg_bytes) ? 1 : 0;
   info.xcd_run = (int)std::min<int64_t>(xcd_run_for((int)coll), INT32_MAX);
+  info.list_schedule = d.sched.list ? 1 : 0;
   *out = info;
   return PAT_OK;
 }
@@ -1218,7 +1243,8 @@ pat_status_t pat_step_clock(pat_collective_t coll, int nranks, size_t count, pat
   std::lock_guard<std::mutex> lock(g_mu);
   int device = 0;
   HIP_TRY(hipGetDevice(&device));
-  auto it = g_plans.find(PlanKey((int)coll, nranks, (int64_t)count, (int)dtype, budget_now(), order_now(), device));
+  auto it = g_plans.find(
+      PlanKey((int)coll, nranks, (int64_t)count, (int)dtype, budget_now(), order_now(), device, aggregation_now()));
   if (it == g_plans.end() || !it->second->step_clock || it->second->stamp_wgs == 0) return PAT_ERR_INVALID_ARGUMENT;
   Plan* p = it->second.get();
   *workgroups = p->stamp_wgs;

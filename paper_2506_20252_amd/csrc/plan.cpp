@@ -2,6 +2,8 @@
 #include "plan.hpp"
 
 #include <algorithm>
+#include <set>
+#include <tuple>
 #include <utility>
 
 namespace pat {
@@ -85,6 +87,7 @@ static bool needs_slot(int N, int p) {
 }
 
 int32_t SlotMap::index(int p) const {
+  if (!table.empty()) return p >= 0 && p < (int)table.size() ? table[p] : -1;
   if (!needs_slot(N, p)) return -1;
   const int D = p & -p;
   return base[ceil_log2(D)] + p / std::max(2 * D, M);
@@ -113,11 +116,141 @@ SlotMap make_slot_map(int N, int L, int M) {
   return m;
 }
 
+Schedule make_list_schedule(int N, int K, SlotMap* slots) {
+  Schedule s;
+  s.N = N;
+  s.list = true;
+  s.T = std::max(1, K);
+  s.M = 0;
+  slots->table.clear();
+  if (N <= 1) return s;
+  const int L = ceil_log2(N);
+  s.L = L;
+  K = std::max(1, K);
+  // Children of every position, farthest first; sub-tree sizes (children sit
+  // at larger positions).
+  std::vector<std::vector<std::pair<int, int>>> kids(N);
+  for (int p = 0; p < N; ++p) {
+    const int reach = p == 0 ? (1 << L) : (p & -p);
+    for (int d = reach / 2; d >= 1; d /= 2)
+      if (p + d < N) kids[p].emplace_back(p + d, d);
+  }
+  std::vector<int64_t> sz(N, 1);
+  for (int p = N - 1; p >= 0; --p)
+    for (const auto& [c, d] : kids[p]) sz[p] += sz[c];
+  // Ready edges by the log2 of their distance, in priority order (larger
+  // sub-tree first, then smaller position); apart, those into nodes that
+  // forward and those into leaves.
+  using Key = std::pair<int64_t, int>;  // (-size of the child's sub-tree, sender)
+  std::vector<std::set<Key>> fwd(L), leaf(L);
+  auto add_ready = [&](int p, const std::vector<int>& nxt) {
+    if (nxt[p] >= (int)kids[p].size()) return;
+    const auto [c, d] = kids[p][nxt[p]];
+    const int l = ceil_log2(d);
+    (kids[c].empty() ? leaf : fwd)[l].insert(Key(-sz[c], p));
+  };
+  std::vector<int> nxt(N, 0), color(N, -1), dim_of(N, -1);
+  std::vector<std::vector<char>> used(L);
+  std::vector<int> cap(L, 0), occ(L, 0);
+  add_ready(0, nxt);
+  int sent = 0;
+  while (sent < N - 1) {
+    int best_l = -1;
+    std::pair<int64_t, int> best_key(-1, -1);
+    std::vector<int> best_take;
+    for (int l = L - 1; l >= 0; --l) {
+      // merge the two priority orders; into forwarding nodes only while the slot has room
+      std::vector<int> take;
+      int64_t weight = 0;
+      int room = K - occ[l];
+      auto f = fwd[l].begin(), g = leaf[l].begin();
+      while ((int)take.size() < K) {
+        const bool fok = f != fwd[l].end() && room > 0;
+        const bool gok = g != leaf[l].end();
+        if (!fok && !gok) break;
+        if (fok && (!gok || *f < *g)) {
+          take.push_back(f->second);
+          weight += -f->first;
+          --room;
+          ++f;
+        } else {
+          take.push_back(g->second);
+          weight += -g->first;
+          ++g;
+        }
+      }
+      if (take.empty()) continue;
+      const std::pair<int64_t, int> key(weight, (int)take.size());
+      if (key > best_key) {
+        best_key = key;
+        best_l = l;
+        best_take = take;
+      }
+    }
+    if (best_l < 0) {
+      s.steps.clear();
+      s.pos.clear();
+      return s;
+    }
+    std::sort(best_take.begin(), best_take.end());
+    StepSpec st{1 << best_l, (int32_t)best_take.size(), (int32_t)s.pos.size()};
+    std::vector<int> done_senders;
+    for (int p : best_take) {
+      const auto [c, d] = kids[p][nxt[p]];
+      (kids[c].empty() ? leaf : fwd)[best_l].erase(Key(-sz[c], p));
+      s.pos.push_back(p);
+      ++nxt[p];
+      ++sent;
+      if (!kids[c].empty()) {  // c keeps the chunk in the slot of distance d until its last forward
+        auto& u = used[best_l];
+        int col = 0;
+        while (col < (int)u.size() && u[col]) ++col;
+        if (col == (int)u.size()) u.push_back(0);
+        u[col] = 1;
+        color[c] = col;
+        dim_of[c] = best_l;
+        cap[best_l] = std::max(cap[best_l], col + 1);
+        ++occ[best_l];
+        add_ready(c, nxt);
+      }
+      add_ready(p, nxt);
+      if (nxt[p] == (int)kids[p].size()) done_senders.push_back(p);
+    }
+    // a sender that has forwarded to all of its children frees its entry after the step
+    for (int p : done_senders)
+      if (dim_of[p] >= 0) {
+        used[dim_of[p]][color[p]] = 0;
+        --occ[dim_of[p]];
+      }
+    s.steps.push_back(st);
+  }
+  slots->N = N;
+  slots->L = L;
+  slots->M = 0;
+  slots->base.assign(L, 0);
+  slots->cap.assign(L, 0);
+  slots->dims = 0;
+  int32_t acc = 0;
+  for (int l = 0; l < L; ++l) {
+    slots->base[l] = acc;
+    slots->cap[l] = cap[l];
+    acc += cap[l];
+    if (cap[l] > 0) ++slots->dims;
+  }
+  slots->entries = acc;
+  slots->table.assign(N, -1);
+  for (int p = 0; p < N; ++p)
+    if (dim_of[p] >= 0) slots->table[p] = slots->base[dim_of[p]] + color[p];
+  return s;
+}
+
 static int elem_bytes(int dtype) { return dtype == 2 ? 2 : 4; }
 
-bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out) {
+bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out,
+                    int aggregation) {
   if (coll < 0 || coll > 1 || N < 1 || count < 0 || dtype < 0 || dtype > 2) return false;
   if (order != kFarFirst && order != kCloseFirst) return false;
+  if (aggregation != kAggPow2 && aggregation != kAggBudget) return false;
   PlanDesc d;
   d.coll = coll;
   d.order = order;
@@ -152,6 +285,20 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, in
 
   const int M = d.sched.M;
   d.slots = make_slot_map(N, d.sched.L, M);
+  // With the budget's chunks per step not a power of two, a list schedule may
+  // need fewer steps; it replaces the power-of-two one only then.
+  if (aggregation == kAggBudget && N > 2 && d.pieces == 1) {
+    const int64_t K = c_slot > 0 ? int64_t(double(budget) / c_slot) : 1;
+    if (K >= 2 && K < int64_t(N) && (int)d.sched.steps.size() > d.sched.L) {
+      SlotMap ls;
+      Schedule alt = make_list_schedule(N, (int)std::min<int64_t>(K, N), &ls);
+      if (!alt.steps.empty() && alt.steps.size() < d.sched.steps.size()) {
+        d.sched = std::move(alt);
+        d.slots = std::move(ls);
+        d.max_k = max_chunks_per_step(d.sched);
+      }
+    }
+  }
   const auto& S = d.sched;
   if (coll == 0) {
     for (const auto& st : S.steps) {

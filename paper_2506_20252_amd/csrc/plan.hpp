@@ -27,6 +27,7 @@ struct StepSpec {
 
 struct Schedule {
   int N = 0, L = 0, t = 0, T = 1, M = 1;
+  bool list = false;            // a list schedule (make_list_schedule): K chunks per step, T = K, t and M unused
   std::vector<StepSpec> steps;  // all-gather order
   std::vector<int32_t> pos;     // sender positions, step after step
 };
@@ -46,6 +47,21 @@ Schedule make_schedule(int N, int t, int order = kFarFirst);
 
 int max_chunks_per_step(const Schedule& s);
 
+struct SlotMap;
+
+// List schedule for K chunks per step (any K >= 1), one distance per step, as
+// the paper's steps are: every rank sends to one peer r + d per step.  Each
+// step takes the distance whose ready edges carry the largest sub-trees (ties:
+// the farther distance), then up to K of its ready edges, largest sub-trees
+// first; a node forwards its children farthest first, so the reduce-scatter
+// adds them nearest first, the same association as the power-of-two
+// schedule's.  An edge into a node that forwards needs room in the slot of
+// its distance: at most K chunks per slot, a slot entry freed after the step
+// of its chunk's last forward.  Entries are assigned lowest-free-first, and
+// `slots` gets the resulting per-position table.  Returns an empty schedule
+// with N > 1 if no step can be formed (cannot happen for K >= 1).
+Schedule make_list_schedule(int N, int K, SlotMap* slots);
+
 // Intermediate-buffer layout of one rank.  A node of a tree that forwards
 // (all-gather) or accumulates (reduce-scatter) keeps the chunk in the slot of
 // the distance D it arrived on / will leave on, D = lowest set bit of its
@@ -58,6 +74,7 @@ struct SlotMap {
   std::vector<int32_t> cap;   // by log2 D: entries of that slot
   int32_t entries = 0;        // chunk-sized entries per rank
   int dims = 0;               // distances that need a slot
+  std::vector<int32_t> table; // list schedules: entry of each position (-1: none); empty: the formula
   // Entry index of position p, or -1 if that node neither forwards nor accumulates.
   int32_t index(int p) const;
 };
@@ -82,8 +99,14 @@ struct PlanDesc {
   double alg_bytes = 0.0;
 };
 
+// Aggregation rule: the paper's power-of-two number of parallel sub-trees,
+// or any number of chunks per step the budget holds (the list schedule where
+// it takes fewer steps than the power-of-two one).
+enum Aggregation : int { kAggPow2 = 0, kAggBudget = 1 };
+
 // Budget in bytes per slot.  Returns false for unsupported arguments.
-bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out);
+bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out,
+                    int aggregation = kAggPow2);
 
 // Dependencies of every entry of d.entries for dataflow execution (one piece
 // in execution order): for each of the two buffers an edge touches, the

@@ -54,11 +54,15 @@ PAT_FUSION_OFF = 1
 PAT_FUSION_ON = 2
 FUSIONS = {"auto": PAT_FUSION_AUTO, "off": PAT_FUSION_OFF, "on": PAT_FUSION_ON}
 
+PAT_AGGREGATION_POW2 = 0
+PAT_AGGREGATION_BUDGET = 1
+AGGREGATIONS = {"pow2": PAT_AGGREGATION_POW2, "budget": PAT_AGGREGATION_BUDGET}
+
 # Every function include/pat.h declares.
 EXPORTS = (
     "pat_allgather", "pat_reducescatter", "pat_reducescatter_noalloc", "pat_set_buffer_bytes", "pat_get_buffer_bytes",
     "pat_set_exec_mode", "pat_get_exec_mode", "pat_set_linear_order", "pat_get_linear_order",
-    "pat_set_top_fusion", "pat_get_top_fusion",
+    "pat_set_top_fusion", "pat_get_top_fusion", "pat_set_aggregation", "pat_get_aggregation",
     "pat_set_barrier_timeout_us", "pat_plan_info",
     "pat_plan_steps", "pat_trace_start", "pat_trace_read", "pat_step_clock", "pat_cache_stats",
     "pat_check_device_status", "pat_last_hip_error", "pat_status_string",
@@ -76,6 +80,7 @@ class pat_plan_info_t(ctypes.Structure):
         ("slot_bytes_total", ctypes.c_size_t), ("alg_bytes", ctypes.c_double),
         ("bus_bytes_per_rank", ctypes.c_double), ("fused_steps", ctypes.c_int),
         ("launches_per_op", ctypes.c_int), ("streaming", ctypes.c_int), ("xcd_run", ctypes.c_int),
+        ("list_schedule", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -114,6 +119,8 @@ def lib():
             "pat_get_linear_order": ([], ctypes.c_int),
             "pat_set_top_fusion": ([ctypes.c_int], ctypes.c_int),
             "pat_get_top_fusion": ([], ctypes.c_int),
+            "pat_set_aggregation": ([ctypes.c_int], ctypes.c_int),
+            "pat_get_aggregation": ([], ctypes.c_int),
             "pat_set_barrier_timeout_us": ([ctypes.c_uint32], ctypes.c_int),
             "pat_plan_info": ([ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                                ctypes.POINTER(pat_plan_info_t)], ctypes.c_int),
@@ -302,6 +309,14 @@ def pat_set_top_fusion(mode):
 
 def pat_get_top_fusion():
     return int(lib().pat_get_top_fusion())
+
+
+def pat_set_aggregation(mode):
+    return lib().pat_set_aggregation(AGGREGATIONS[mode] if isinstance(mode, str) else int(mode))
+
+
+def pat_get_aggregation():
+    return int(lib().pat_get_aggregation())
 
 
 def pat_set_linear_order(order):

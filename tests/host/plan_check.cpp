@@ -6,7 +6,10 @@
 // (dataflow_deps) symbolically: edges execute in orders that respect nothing
 // but their counters (shuffled, and latest step first), and every transfer
 // must find what the schedule promises -- the chunk a sender forwards, the
-// partial sums a receiver adds -- with no edge left unable to run.
+// partial sums a receiver adds -- with no edge left unable to run.  Plans with
+// PAT_AGGREGATION_BUDGET (list schedules where they are shorter) get the same
+// checks, plus: never more steps than the power-of-two plan, at most K =
+// budget / chunk bytes chunks per step and per slot.
 #include <algorithm>
 #include <cstdint>
 #include <cstdio>
@@ -102,19 +105,41 @@ const char* simulate_dataflow(const pat::PlanDesc& d, uint32_t seed, bool latest
 }  // namespace
 
 int main() {
-  long plans = 0, dataflow_runs = 0;
-  const size_t budgets[] = {16, 4096, 65536, size_t(8) << 20};
+  long plans = 0, dataflow_runs = 0, list_plans = 0;
+  // 204, 340 and 476 bytes are 3, 5 and 7 chunks of 17 four-byte elements: with
+  // PAT_AGGREGATION_BUDGET they bring in the list schedule
+  const size_t budgets[] = {16, 204, 340, 476, 4096, 65536, size_t(8) << 20};
   for (int N = 1; N <= 300; ++N) {
     for (int order = 0; order < 2; ++order) {
       for (size_t budget : budgets) {
         for (int coll = 0; coll < 2; ++coll) {
           for (int64_t count : {int64_t(1), int64_t(17), int64_t(1000)}) {
+           for (int agg = 0; agg < 2; ++agg) {
+            if (agg == 1 && (order == 1 || count != 17)) continue;
             pat::PlanDesc d;
-            if (!pat::make_plan_desc(coll, N, count, coll ? 2 : 1, budget, order, &d)) {
-              std::fprintf(stderr, "plan failed N=%d budget=%zu order=%d\n", N, budget, order);
+            if (!pat::make_plan_desc(coll, N, count, coll ? 2 : 1, budget, order, &d, agg)) {
+              std::fprintf(stderr, "plan failed N=%d budget=%zu order=%d agg=%d\n", N, budget, order, agg);
               return 1;
             }
             ++plans;
+            if (agg == 1) {
+              pat::PlanDesc p2;
+              pat::make_plan_desc(coll, N, count, coll ? 2 : 1, budget, order, &p2, 0);
+              const int64_t K = int64_t(budget / (size_t(count) * 4));
+              if (d.exec.size() > p2.exec.size() || (d.sched.list && d.max_k > K)) {
+                std::fprintf(stderr, "N=%d budget=%zu: list schedule %zu steps (max %d chunks) vs %zu\n", N, budget,
+                             d.exec.size(), d.max_k, p2.exec.size());
+                return 1;
+              }
+              if (d.sched.list) {
+                ++list_plans;
+                for (int c = 0; c < (int)d.slots.cap.size(); ++c)
+                  if (d.slots.cap[c] > K) {
+                    std::fprintf(stderr, "N=%d budget=%zu: %d chunks in one slot\n", N, budget, d.slots.cap[c]);
+                    return 1;
+                  }
+              }
+            }
             if (N == 1) continue;
             if ((int)d.entries.size() != N - 1) {
               std::fprintf(stderr, "N=%d: %zu entries\n", N, d.entries.size());
@@ -141,17 +166,20 @@ int main() {
             if (N <= 64 && count == 17) {
               for (int mode = 0; mode < 2; ++mode) {
                 if (const char* err = simulate_dataflow(d, uint32_t(N * 7919 + order * 31 + coll), mode == 1)) {
-                  std::fprintf(stderr, "N=%d coll=%d budget=%zu order=%d: %s\n", N, coll, budget, order, err);
+                  std::fprintf(stderr, "N=%d coll=%d budget=%zu order=%d agg=%d: %s\n", N, coll, budget, order, agg,
+                               err);
                   return 1;
                 }
                 ++dataflow_runs;
               }
             }
+           }
           }
         }
       }
     }
   }
-  std::printf("plans checked: %ld, dataflow simulations: %ld\n", plans, dataflow_runs);
+  std::printf("plans checked: %ld (list schedules: %ld), dataflow simulations: %ld\n", plans, list_plans,
+              dataflow_runs);
   return 0;
 }

@@ -465,6 +465,33 @@ def test_persistent_barrier_timeout_is_reported_and_recovers():
              oracle_t(pat.PAT_REDUCESCATTER, n, count, "float32"))
 
 
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("n,K", [(12, 3), (24, 5), (64, 3), (100, 6), (128, 7)])
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+def test_list_schedule_of_budget_aggregation(n, K, dtype, mode):
+    """PAT_AGGREGATION_BUDGET with a budget of K chunks per step: the list
+    schedule (fewer steps than the power-of-two one here) against the oracle,
+    all-gather bit-exact, reduce-scatter bit-exact against the PAT order."""
+    count, seed = 1000, 0x1157 + n * 7 + K
+    pat.check(pat.pat_set_aggregation("budget"))
+    try:
+        for coll in ("ag", "rs"):
+            slot = 4 if (coll == "rs" or dtype != "bfloat16") else 2
+            pat.check(pat.pat_set_buffer_bytes(K * count * slot))
+            code = pat.PAT_ALLGATHER if coll == "ag" else pat.PAT_REDUCESCATTER
+            st, info = pat.pat_plan_info(code, n, count, dtype)
+            assert info["list_schedule"] == 1, info
+            if coll == "ag":
+                got, host_in = run_ag(n, count, dtype, seed, mode=mode)
+                np.testing.assert_array_equal(got, D.allgather(host_in))
+            else:
+                got = run_rs(n, count, dtype, seed, mode=mode)
+                check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed), dtype, 0)
+    finally:
+        pat.check(pat.pat_set_aggregation("pow2"))
+        pat.check(pat.pat_set_buffer_bytes(0))
+
+
 def test_dataflow_wait_timeout_is_reported_and_recovers():
     """Failure handling forced from the host: a 1 us limit on the dataflow
     kernel's bounded waits for the buffers of earlier steps (1 MiB chunks:

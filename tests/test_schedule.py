@@ -4,6 +4,7 @@ symbolic execution of the library's step tables, slot indices included.
 Integer work: every comparison is exact.  No GPU needed.
 """
 
+import numpy as np
 import pytest
 from hypothesis import given, settings, strategies as hs
 
@@ -442,4 +443,68 @@ def test_vector_path_reported_by_plan_info(coll, dtype):
                 want = 1 if whole else 2 if holds_one else 0
                 assert info["vector_path"] == want, (budget, count, lens)
     finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+
+
+@pytest.mark.parametrize("n", [5, 6, 7, 12, 13, 16, 24, 33, 64, 100, 128])
+@pytest.mark.parametrize("K", [3, 5, 6, 7])
+def test_list_schedule_of_budget_aggregation(n, K):
+    """PAT_AGGREGATION_BUDGET with a budget of K chunks per step (K not a
+    power of two): where the library takes its list schedule, the tables
+    never need more steps than the power-of-two schedule, never carry more
+    than K chunks per step or hold more than K per slot, pass the symbolic
+    execution, and -- run by the oracle's own step executors, which check
+    every transfer -- deliver every chunk exactly once and sum in the same
+    association as the reversed-tree closed form."""
+    count, esize = 17, 4
+    rng = np.random.default_rng(n * 10 + K)
+    pat.check(pat.pat_set_buffer_bytes(K * count * esize))
+    try:
+        pat.check(pat.pat_set_aggregation("pow2"))
+        pow2 = {c: pat.pat_plan_info(c, n, count, "float32")[1]["steps"]
+                for c in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER)}
+        pat.check(pat.pat_set_aggregation("budget"))
+        for coll in (pat.PAT_ALLGATHER, pat.PAT_REDUCESCATTER):
+            st, info = pat.pat_plan_info(coll, n, count, "float32")
+            st, steps, entries = pat.pat_plan_steps(coll, n, count, "float32")
+            assert len(steps) == info["steps"] <= pow2[coll]
+            assert max(k for _, k in steps) <= K
+            if coll == pat.PAT_ALLGATHER:
+                run_symbolic_allgather(n, steps, entries)  # its peak sums every slot of a rank
+                ag_steps, j = [], 0
+                for d, k in steps:
+                    ag_steps.append((d, sorted(e[0] for e in entries[j:j + k])))
+                    j += k
+                x = rng.integers(-2**31, 2**31, size=(n, 3), dtype=np.int64).astype(np.int32)
+                recv, stats = opat.allgather(x, 0, steps=ag_steps)
+                assert (recv == np.broadcast_to(x[None], (n,) + x.shape)).all()
+                assert max(stats["peak_per_dim"].values(), default=0) <= K
+                xf = rng.standard_normal((n, n, 5)).astype(np.float32)
+                out, stats = opat.reducescatter(xf, 0, "float32", steps=ag_steps)
+                assert (out.view(np.uint32) == opat.reducescatter_closed_form(xf, "float32").view(np.uint32)).all()
+                assert max(stats["peak_per_dim"].values(), default=0) <= K
+                list_ag = info["list_schedule"]
+            else:
+                run_symbolic_reducescatter(n, steps, entries)
+                assert info["list_schedule"] == list_ag
+                assert info["fused_steps"] == 0 or not info["list_schedule"]
+    finally:
+        pat.check(pat.pat_set_aggregation("pow2"))
+        pat.check(pat.pat_set_buffer_bytes(0))
+
+
+def test_list_schedule_shortens_non_power_of_two_budgets():
+    """The point of the list schedule: with 3 chunks per step, N = 128 needs
+    fewer than the 64 steps of T = 2; with a power-of-two budget and a
+    power-of-two N nothing changes."""
+    pat.check(pat.pat_set_aggregation("budget"))
+    try:
+        pat.check(pat.pat_set_buffer_bytes(3 * 256))
+        st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, 128, 64, "float32")
+        assert info["list_schedule"] == 1 and info["steps"] < 64 and info["max_chunks_per_step"] <= 3
+        pat.check(pat.pat_set_buffer_bytes(4 * 256))
+        st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, 128, 64, "float32")
+        assert info["list_schedule"] == 0 and info["steps"] == 33
+    finally:
+        pat.check(pat.pat_set_aggregation("pow2"))
         pat.check(pat.pat_set_buffer_bytes(0))
