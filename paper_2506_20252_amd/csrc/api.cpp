@@ -65,6 +65,14 @@ int aggregation_now() {
   return PAT_AGGREGATION_POW2;
 }
 
+// Pipelined pieces (tuning): PAT_PIECE_PIPELINE=1 when a plan is made cuts a
+// chunk larger than the budget into pieces of half the budget, alternating
+// between two halves of every slot, and runs two pieces' steps per launch.
+bool pipeline_now() {
+  const char* e = std::getenv("PAT_PIECE_PIPELINE");
+  return e && e[0] == '1';
+}
+
 int fusion_now() {
   if (g_fusion >= 0) return g_fusion;
   if (const char* e = std::getenv("PAT_TOP_FUSION")) {
@@ -219,6 +227,7 @@ struct HostPlan {
   int64_t xcd_run = 1;     // step kernels: work items per XCD run (0: a contiguous eighth)
   double alg_bytes = 0.0;  // algorithmic bytes of one operation
   int64_t slot_chunk_stride = 0, slot_rank_stride = 0, rootacc_stride = 0;
+  int64_t slot_half_bytes = 0, root_half_bytes = 0;  // pipelined pieces: offsets of the second halves
 };
 
 struct Plan {
@@ -350,6 +359,7 @@ bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, 
       ds.k = st.k;
       ds.entry0 = st.first;
       ds.first = j == 0 ? 1 : 0;
+      ds.half = d.pipelined ? piece % 2 : 0;
       ds.back = (int16_t)back;
       ds.e0 = e0;
       ds.V = V;
@@ -388,7 +398,8 @@ int aligned_path(const bool (&has)[3]) { return has[1] ? 1 : has[2] ? 2 : 0; }
 // Schedule tables and slot layout of a plan (host memory only).
 pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size_t budget, int order, int agg,
                             HostPlan* h) {
-  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &h->desc, agg)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, count, (int)dt, budget, order, &h->desc, agg, pipeline_now()))
+    return PAT_ERR_INVALID_ARGUMENT;
   const pat::PlanDesc& d = h->desc;
   for (int path = 0; path < 3; ++path) {
     const pat::Variant v = variant_for(coll, dt, path);
@@ -403,6 +414,12 @@ pat_status_t make_host_plan(int coll, int N, int64_t count, pat_dtype_t dt, size
   h->slot_chunk_stride = (int64_t)entry_stride(size_t(d.piece_elems) * d.esize_slot);
   h->slot_rank_stride = h->slot_chunk_stride * d.slots.entries;
   h->rootacc_stride = (coll == 1 && dt == PAT_BFLOAT16) ? (int64_t)entry_stride(size_t(d.piece_elems) * 4) : 0;
+  if (d.pipelined) {  // two halves per rank: [half 0 | half 1]
+    h->slot_half_bytes = h->slot_rank_stride;
+    h->slot_rank_stride *= 2;
+    h->root_half_bytes = h->rootacc_stride;
+    h->rootacc_stride *= 2;
+  }
   return PAT_OK;
 }
 
@@ -654,6 +671,8 @@ pat::KCtx make_ctx(const HostPlan& h, int vi, const void* const* d_send, void* c
   cx.slot_chunk_stride = h.slot_chunk_stride;
   cx.slot_rank_stride = h.slot_rank_stride;
   cx.rootacc_stride = h.rootacc_stride;
+  cx.slot_half_bytes = h.slot_half_bytes;
+  cx.root_half_bytes = h.root_half_bytes;
   cx.esize = (int64_t)h.desc.esize_in;
   cx.N = N;
   cx.nsteps = (int32_t)h.steps[vi].size();
@@ -709,6 +728,40 @@ hipError_t enqueue_stream(const HostPlan& h, int coll, pat_dtype_t dt, int vi, c
                           const pat::TreeRange& tr, hipStream_t q, Trace* trace = nullptr) {
   const pat::Variant var = variant_for(coll, dt, vi);
   const auto& steps = h.steps[vi];
+  if (h.desc.pipelined) {
+    // Piece p starts at launch (p / 2) * S + p % 2 (S steps per piece): two
+    // pieces in flight, one step apart, in the two slot halves; a piece
+    // starts its half only once the piece two before it has finished.
+    const int S = (int)h.desc.exec.size(), P = h.desc.pieces;
+    const int launches = ((P - 1) / 2) * S + (P - 1) % 2 + S;
+    for (int j = 0; j < launches; ++j) {
+      int idx[2], n = 0;
+      for (int p = 0; p < P && n < 2; ++p) {
+        const int start = (p / 2) * S + p % 2;
+        if (j >= start && j < start + S) idx[n++] = p * S + (j - start);
+      }
+      const bool traced = trace && trace->used < trace->max;
+      if (traced) {
+        const hipError_t e = hipEventRecord(trace->ev[2 * trace->used], q);
+        if (e != hipSuccess) return e;
+      }
+      const hipError_t e =
+          n == 2 ? pat::launch_step2(var, h.streaming, xcd_grain(h.xcd_run), cx, idx[0], steps[idx[0]], idx[1],
+                                     steps[idx[1]], q)
+                 : pat::launch_step(var, h.streaming, xcd_grain(h.xcd_run), cx, steps[idx[0]], q);
+      if (e != hipSuccess) return e;
+      if (traced) {
+        const int t = trace->used;
+        const hipError_t e2 = hipEventRecord(trace->ev[2 * t + 1], q);
+        if (e2 != hipSuccess) return e2;
+        trace->bytes[t] = launch_bytes(h, vi, idx[0]) + (n == 2 ? launch_bytes(h, vi, idx[1]) : 0.0);
+        trace->kind[t] = 0;
+        trace->step[t] = idx[0];
+        trace->used = t + 1;
+      }
+    }
+    return hipSuccess;
+  }
   const bool fuse = tr.s1 > tr.s0;
   for (int s = 0; s < (int)steps.size(); ++s) {
     const bool traced = trace && trace->used < trace->max;
@@ -1019,7 +1072,8 @@ pat_status_t describe(int coll, int N, size_t count, pat_dtype_t dt, pat::PlanDe
     order = order_now();
     agg = aggregation_now();
   }
-  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, order, d, agg)) return PAT_ERR_INVALID_ARGUMENT;
+  if (!pat::make_plan_desc(coll, N, (int64_t)count, (int)dt, budget, order, d, agg, pipeline_now()))
+    return PAT_ERR_INVALID_ARGUMENT;
   return PAT_OK;
 }
 
@@ -1154,6 +1208,7 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
     fused_range(d, V, fusion_now(), &s0, &s1, &tile);
     info.fused_steps = s1 - s0;
     info.launches_per_op = int(d.exec.size()) * d.pieces - (s1 > s0 ? s1 - s0 - 1 : 0);
+    if (d.pipelined) info.launches_per_op = ((d.pieces - 1) / 2) * int(d.exec.size()) + (d.pieces - 1) % 2 + int(d.exec.size());
   }
   info.streaming = streaming_for(d.alg_bytes) ? 1 : 0;
   info.xcd_run = (int)std::min<int64_t>(xcd_run_for((int)coll), INT32_MAX);

@@ -54,6 +54,9 @@ struct DevStep {
   int32_t df_edges;        // dataflow execution: whole edges per work item (chunks under one tile;
                            // 0: the item is df_tiles tiles of one edge)
   int32_t df_tiles;        // dataflow execution: tiles of one edge per work item
+  int32_t half;            // pipelined pieces: the half of every slot (and root accumulator) this
+                           // piece uses (0 otherwise)
+  int32_t pad;
 };
 
 }  // namespace pat

@@ -264,10 +264,11 @@ struct AgOp {
     const char* send_r = (const char*)cx.send[r];
     char* recv_peer = (char*)cx.recv[peer];
     char* recv_r = (char*)cx.recv[r];
+    char* const slots = cx.slots + st.half * cx.slot_half_bytes;
     Edge e;
-    e.src = en.a == kUser ? send_r + piece : cx.slots + r * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.src = en.a == kUser ? send_r + piece : slots + r * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
     e.dst = recv_peer + c * chunk + piece;
-    e.dst2 = en.b >= 0 ? cx.slots + peer * cx.slot_rank_stride + en.b * cx.slot_chunk_stride : nullptr;
+    e.dst2 = en.b >= 0 ? slots + peer * cx.slot_rank_stride + en.b * cx.slot_chunk_stride : nullptr;
     e.dst3 = (st.first && en.p == 0 && cx.own_copy) ? recv_r + r * chunk + piece : nullptr;
     return e;
   }
@@ -559,11 +560,13 @@ struct RsOp {
     const char* send_child = (const char*)cx.send[child];
     const char* send_r = (const char*)cx.send[r];
     char* const recv_r = (char*)cx.recv[r] + st.e0 * R::kInElem;
-    char* const root_acc = R::kSeparateRoot ? cx.rootacc + r * cx.rootacc_stride : recv_r;
-    char* const slots_r = cx.slots + r * cx.slot_rank_stride;
+    char* const root_acc =
+        R::kSeparateRoot ? cx.rootacc + st.half * cx.root_half_bytes + r * cx.rootacc_stride : recv_r;
+    char* const slots = cx.slots + st.half * cx.slot_half_bytes;
+    char* const slots_r = slots + r * cx.slot_rank_stride;
     Edge e;
     e.child_in = en.a == kUser;
-    e.child = e.child_in ? send_child + uoff : cx.slots + child * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
+    e.child = e.child_in ? send_child + uoff : slots + child * cx.slot_rank_stride + en.a * cx.slot_chunk_stride;
     e.own_in = en.b == kUser;
     e.own = e.own_in ? send_r + uoff : en.b == kRoot ? root_acc : slots_r + en.b * cx.slot_chunk_stride;
     e.dst_final = R::kSeparateRoot && en.c == kRootFinal;
@@ -829,6 +832,26 @@ __global__ __launch_bounds__(kThreads) void step_kernel(KCtx cx, DevStep st, int
   // One call site for Op::run: a second inlined copy of the bf16 op pushed
   // the compiler into scratch memory.
   for (; item < st.items; item += stride) Op::run(cx, st, item);
+}
+
+// Two independent launch-level steps in one launch (pipelined pieces): the
+// items of step ia, then those of step ib, read from the device step table
+// (one call site for Op::run).  Work-item order as in step_kernel, over the
+// launch's items.
+template <class Op>
+__global__ __launch_bounds__(kThreads) void step2_kernel(KCtx cx, int ia, int ib, int64_t na, int64_t total,
+                                                         int64_t grain) {
+  int64_t item = blockIdx.x, stride = gridDim.x;
+  if (grain > 1) {
+    const int64_t x = blockIdx.x % 8, j = blockIdx.x / 8;
+    item = (j / grain) * 8 * grain + x * grain + j % grain;
+    stride = total;  // at most one item per workgroup
+  }
+  for (; item < total; item += stride) {
+    const bool first = item < na;
+    const DevStep st = cx.steps[first ? ia : ib];
+    Op::run(cx, st, first ? item : item - na);
+  }
 }
 
 // Fused range of steps: one workgroup per (tree, tile of its chunk) runs the
@@ -1234,6 +1257,25 @@ hipError_t launch_step_t(const KCtx& cx, const DevStep& st, int64_t grain, hipSt
 }
 
 template <class Op>
+hipError_t launch_step2_t(const KCtx& cx, int ia, int64_t na, int ib, int64_t nb, int64_t grain, hipStream_t stream) {
+  const int64_t items = na + nb;
+  if (items <= 0) return hipSuccess;
+  const int64_t cap = int64_t(1) << 30;
+  unsigned grid = (unsigned)(items < cap ? items : cap);
+  if (grain > 1) {
+    grain = grain < (items + 7) / 8 ? grain : (items + 7) / 8;
+    const int64_t run = 8 * grain;
+    const int64_t g = (items + run - 1) / run * run;
+    if (g <= cap)
+      grid = (unsigned)g;
+    else
+      grain = 1;
+  }
+  hipLaunchKernelGGL(step2_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx, ia, ib, na, items, grain);
+  return hipGetLastError();
+}
+
+template <class Op>
 hipError_t launch_persistent_t(const KCtx& cx, int grid, hipStream_t stream) {
   hipLaunchKernelGGL(persistent_kernel<Op>, dim3(grid), dim3(kThreads), 0, stream, cx);
   return hipGetLastError();
@@ -1339,6 +1381,13 @@ hipError_t launch_step(Variant v, bool streaming, int64_t grain, const KCtx& cx,
 #define PAT_STEP(OP) launch_step_t<PAT_UNPAREN OP>(cx, st, grain, stream)
   PAT_DISPATCH(v, streaming, PAT_STEP)
 #undef PAT_STEP
+}
+
+hipError_t launch_step2(Variant v, bool streaming, int64_t grain, const KCtx& cx, int ia, const DevStep& a, int ib,
+                        const DevStep& b, hipStream_t stream) {
+#define PAT_STEP2(OP) launch_step2_t<PAT_UNPAREN OP>(cx, ia, a.items, ib, b.items, grain, stream)
+  PAT_DISPATCH(v, streaming, PAT_STEP2)
+#undef PAT_STEP2
 }
 
 template <class Op>

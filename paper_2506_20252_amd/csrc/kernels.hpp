@@ -42,6 +42,8 @@ struct KCtx {
   unsigned* counters;         // dataflow execution: [N][counter_stride] completed tiles per buffer (zero
                               // between launches)
   int64_t counter_stride;     // slot entries per rank + 1 (the own chunk's accumulator)
+  int64_t slot_half_bytes;    // pipelined pieces: offset of a slot area's second half (0 otherwise)
+  int64_t root_half_bytes;    // pipelined pieces: offset of a root accumulator's second half
 };
 
 // Words of the persistent kernel's counter area for `nsteps` launch-level steps.
@@ -86,6 +88,11 @@ bool variant_partial_items(Variant v);
 // eighth item; large: a contiguous eighth of the step; see step_kernel).
 hipError_t launch_step(Variant v, bool streaming, int64_t grain, const KCtx& cx, const DevStep& st,
                        hipStream_t stream);
+// Pipelined pieces: two launch-level steps of the device step table (indices
+// ia, ib; different pieces and slot halves, hence independent) in one launch,
+// the items of step ia first.
+hipError_t launch_step2(Variant v, bool streaming, int64_t grain, const KCtx& cx, int ia, const DevStep& a, int ib,
+                        const DevStep& b, hipStream_t stream);
 // Fused range: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
 struct TreeRange {

@@ -247,7 +247,7 @@ Schedule make_list_schedule(int N, int K, SlotMap* slots) {
 static int elem_bytes(int dtype) { return dtype == 2 ? 2 : 4; }
 
 bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out,
-                    int aggregation) {
+                    int aggregation, bool pipeline) {
   if (coll < 0 || coll > 1 || N < 1 || count < 0 || dtype < 0 || dtype > 2) return false;
   if (order != kFarFirst && order != kCloseFirst) return false;
   if (aggregation != kAggPow2 && aggregation != kAggBudget) return false;
@@ -272,9 +272,14 @@ bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, in
   d.sched = make_schedule(N, t, order);
   d.max_k = max_chunks_per_step(d.sched);
 
-  // A chunk larger than the budget is processed in pieces (T = 1 then).
+  // A chunk larger than the budget is processed in pieces (T = 1 then); with
+  // the pipeline, pieces of half the budget, two of them in flight.
   d.pieces = 1;
   d.piece_elems = count;
+  if (pipeline && c_slot > double(budget) && budget >= 2 * size_t(d.esize_slot)) {
+    d.pipelined = true;
+    budget /= 2;
+  }
   if (c_slot > double(budget)) {
     int64_t pe = int64_t(budget / size_t(d.esize_slot));
     if (pe <= 0) return false;

@@ -95,6 +95,7 @@ struct PlanDesc {
   std::vector<StepSpec> exec;      // execution order (reduce-scatter: reversed)
   int pieces = 1;
   int64_t piece_elems = 0;
+  bool pipelined = false;  // pieces of half the budget, alternating between two halves of every slot
   int max_k = 0;
   double alg_bytes = 0.0;
 };
@@ -105,8 +106,11 @@ struct PlanDesc {
 enum Aggregation : int { kAggPow2 = 0, kAggBudget = 1 };
 
 // Budget in bytes per slot.  Returns false for unsupported arguments.
+// pipeline: a chunk larger than the budget is cut into pieces of half the
+// budget, piece p using half p % 2 of every slot, so that two pieces can be
+// in flight at once (their steps one apart); no effect when the chunk fits.
 bool make_plan_desc(int coll, int N, int64_t count, int dtype, size_t budget, int order, PlanDesc* out,
-                    int aggregation = kAggPow2);
+                    int aggregation = kAggPow2, bool pipeline = false);
 
 // Dependencies of every entry of d.entries for dataflow execution (one piece
 // in execution order): for each of the two buffers an edge touches, the

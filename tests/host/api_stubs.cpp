@@ -22,6 +22,9 @@ int variant_pack_tile(Variant v) { return v == kAgS4 || v == kAgS2 || v == kRsI3
 
 hipError_t launch_step(Variant, bool, int64_t, const KCtx&, const DevStep&, hipStream_t) { return hipSuccess; }
 hipError_t launch_tree(Variant, bool, const KCtx&, const TreeRange&, hipStream_t) { return hipSuccess; }
+hipError_t launch_step2(Variant, bool, int64_t, const KCtx&, int, const DevStep&, int, const DevStep&, hipStream_t) {
+  return hipSuccess;
+}
 hipError_t launch_persistent(Variant, bool, const KCtx&, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_dataflow(Variant, bool, const KCtx&, bool, int, hipStream_t) { return hipSuccess; }
 hipError_t persistent_capacity(Variant, bool, int* blocks) {

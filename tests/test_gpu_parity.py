@@ -466,7 +466,7 @@ def test_persistent_barrier_timeout_is_reported_and_recovers():
 
 
 @pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
-@pytest.mark.parametrize("n,K", [(12, 3), (24, 5), (64, 3), (100, 6), (128, 7)])
+@pytest.mark.parametrize("n,K", [(12, 2), (24, 5), (64, 3), (100, 6), (128, 7)])
 @pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
 def test_list_schedule_of_budget_aggregation(n, K, dtype, mode):
     """PAT_AGGREGATION_BUDGET with a budget of K chunks per step: the list
@@ -490,6 +490,55 @@ def test_list_schedule_of_budget_aggregation(n, K, dtype, mode):
     finally:
         pat.check(pat.pat_set_aggregation("pow2"))
         pat.check(pat.pat_set_buffer_bytes(0))
+
+
+@pytest.mark.parametrize("mode", ["stream", "graph", "persistent", "dataflow"])
+@pytest.mark.parametrize("dtype", ["int32", "float32", "bfloat16"])
+@pytest.mark.parametrize("n,count,budget", [(5, 1000, 1024), (13, 4100, 4096), (33, 1001, 512)])
+def test_pipelined_pieces(n, count, budget, dtype, mode, monkeypatch):
+    """PAT_PIECE_PIPELINE=1: chunks larger than the budget in pieces of half
+    the budget, alternating between the two halves of every slot, two pieces
+    in flight (their steps one apart, in one launch) -- against the oracle,
+    ragged last pieces included."""
+    pat.check(pat.pat_finalize())
+    monkeypatch.setenv("PAT_PIECE_PIPELINE", "1")
+    pat.check(pat.pat_set_buffer_bytes(budget))
+    seed = 0x9196 + n + count
+    try:
+        for coll in ("ag", "rs"):
+            code = pat.PAT_ALLGATHER if coll == "ag" else pat.PAT_REDUCESCATTER
+            st, info = pat.pat_plan_info(code, n, count, dtype)
+            assert info["pieces"] >= 3
+            if coll == "ag":
+                got, host_in = run_ag(n, count, dtype, seed, mode=mode)
+                np.testing.assert_array_equal(got, D.allgather(host_in))
+            else:
+                got = run_rs(n, count, dtype, seed, mode=mode)
+                check_rs(got, host_rs_inputs(n, count, DIST[dtype], seed), dtype, 0)
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+        monkeypatch.delenv("PAT_PIECE_PIPELINE")
+        pat.check(pat.pat_finalize())
+
+
+def test_workload5_pipelined_pieces_every_element(monkeypatch):
+    """Workload 5 with a 4 MiB budget (half of one float32 chunk): pieces of
+    2 MiB alternating between the two slot halves, two in flight; every
+    output element against the oracle, stream mode."""
+    n, count, seed = 128, 2 * MIB, 0x5041545
+    pat.check(pat.pat_finalize())
+    monkeypatch.setenv("PAT_PIECE_PIPELINE", "1")
+    pat.check(pat.pat_set_buffer_bytes(4 * MIB))
+    try:
+        st, info = pat.pat_plan_info(pat.PAT_REDUCESCATTER, n, count, "bfloat16")
+        assert info["pieces"] == 4 and info["launches_per_op"] == 2 * 127 + 1
+        outs = run_rs_modes(n, count, "bfloat16", seed, ["stream"])
+    finally:
+        pat.check(pat.pat_set_buffer_bytes(0))
+        monkeypatch.delenv("PAT_PIECE_PIPELINE")
+        pat.check(pat.pat_finalize())
+        torch.cuda.empty_cache()
+    compare_rs_full(outs, n, count, "bfloat16", "bf16_normal", seed)
 
 
 def test_dataflow_wait_timeout_is_reported_and_recovers():
