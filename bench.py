@@ -340,6 +340,47 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
     return out
 
 
+def misalign_probe(chunks=500000, reps=20):
+    """Why misaligned receive buffers cost the all-gather: 256-byte chunk
+    copies (libpatceiling.so) at skew 0 and 4 bytes, all chunks in one launch,
+    or even chunks then odd chunks in two launches (lines shared by two chunks
+    then written partly in each launch, as the all-gather's steps fill a
+    receive buffer).  Microseconds per copy of every chunk."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2506_20252_amd", "libpatceiling.so"))
+    fn = lib.pat_ceiling_chunk_copy
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    n = chunks * 256 + 256
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.zeros(n, dtype=torch.uint8, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    rows = []
+    for skew in (0, 4):
+        for split in (False, True):
+            def op():
+                for par in ((0, 1) if split else (-1,)):
+                    if fn(src.data_ptr(), dst.data_ptr(), chunks, skew, par, stream.cuda_stream) != 0:
+                        raise RuntimeError("chunk copy probe: launch failed")
+            op()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                op()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            rows.append({"skew_bytes": skew, "launches": 2 if split else 1, "us": round(us, 2),
+                         "gbps_read_plus_write": round(2 * chunks * 256 / (us * 1e-6) / 1e9, 1)})
+    if not bool(torch.equal(dst[4:4 + chunks * 256], src[4:4 + chunks * 256])):
+        raise RuntimeError("chunk copy probe: wrong copy")
+    print(json.dumps({"metric": "256-byte chunk copies at a skew (why misaligned all-gathers cost more)",
+                      "chunks": chunks, "rows": rows}), flush=True)
+
+
 def budget_sweep(wid, reps, max_slot_bytes=32 << 30, aggregation="pow2"):
     """Time one workload at every aggregation level: the budget is set to the
     bytes of the largest step at T = 1, 2, 4, ... up to full aggregation, so
@@ -696,6 +737,8 @@ def main():
                     help="instead: time the workload at every aggregation level (T = 1 .. full)")
     ap.add_argument("--aggregation", default="pow2", choices=["pow2", "budget"],
                     help="with --budget-sweep: power-of-two sub-trees, or any chunks per step (list schedule)")
+    ap.add_argument("--misalign-probe", action="store_true",
+                    help="instead: 256-byte chunk copies at a skew, one launch or even/odd chunks in two")
     ap.add_argument("--step-clock", action="store_true",
                     help="instead: per-step device clock of the workload's fused launch (PAT_STEP_CLOCK=1)")
     ap.add_argument("--size-sweep", action="store_true",
@@ -718,6 +761,9 @@ def main():
         return
     if args.size_sweep:
         size_sweep()
+        return
+    if args.misalign_probe:
+        misalign_probe()
         return
     if args.step_clock:
         os.environ["PAT_STEP_CLOCK"] = "1"  # read when the plan is made

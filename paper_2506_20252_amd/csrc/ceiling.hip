@@ -45,6 +45,25 @@ __global__ __launch_bounds__(kThreads) void add_kernel(const v4f* a, const v4f* 
   }
 }
 
+// Chunk copies at a skew: chunk c (16 vectors of 16 bytes) of the chunks with
+// c % 2 == parity (every chunk if parity < 0) copies src + 256 c + skew to
+// dst + 256 c + skew with 16-byte vectors at skew-aligned addresses.  Written
+// in two launches (even chunks, then odd ones) the lines that two chunks
+// share are written partly in each, as the all-gather's steps fill a receive
+// buffer chunk by chunk.
+typedef v4u v4u_skewed __attribute__((aligned(4)));
+
+__global__ __launch_bounds__(kThreads) void chunk_copy_kernel(const char* src, char* dst, int64_t chunks, int skew,
+                                                              int parity) {
+  const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t per = parity < 0 ? chunks : (chunks - parity + 1) / 2;
+  if (g >= per * 16) return;
+  const int64_t c = parity < 0 ? g / 16 : (g / 16) * 2 + parity;
+  const int64_t o = c * 256 + skew + (g % 16) * 16;
+  const v4u x = *(const PAT_GLOBAL v4u_skewed*)(src + o);
+  *(PAT_GLOBAL v4u_skewed*)(dst + o) = x;
+}
+
 int launch_check(int64_t n) {
   // bytes must be whole 16-byte vectors and the grid must fit one dimension
   return (n > 0 && (n + kThreads - 1) / kThreads < (int64_t(1) << 31)) ? 0 : (int)hipErrorInvalidValue;
@@ -82,5 +101,21 @@ extern "C" int pat_ceiling_add(const void* a, const void* b, void* c, size_t byt
   if (int e = launch_check(n)) return e;
   hipLaunchKernelGGL(add_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
                      (const v4f*)a, (const v4f*)b, (v4f*)c, n);
+  return (int)hipGetLastError();
+}
+
+// Copies `chunks` 256-byte chunks at byte offset `skew` (0, 4, 8 or 12) of
+// src to the same offsets of dst, every chunk in one launch (parity < 0) or
+// only the chunks of one parity (0 or 1); both buffers must hold
+// 256 * chunks + 16 bytes and be 16-byte aligned.
+extern "C" int pat_ceiling_chunk_copy(const void* src, void* dst, int64_t chunks, int skew, int parity,
+                                      hipStream_t stream) {
+  if (!src || !dst || chunks <= 0 || skew < 0 || skew > 12 || skew % 4 || parity > 1 ||
+      ((uintptr_t)src | (uintptr_t)dst) % 16)
+    return (int)hipErrorInvalidValue;
+  const int64_t per = parity < 0 ? chunks : (chunks - parity + 1) / 2;
+  if (int e = launch_check(per * 16)) return e;
+  hipLaunchKernelGGL(chunk_copy_kernel, dim3((unsigned)((per * 16 + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     stream, (const char*)src, (char*)dst, chunks, skew, parity);
   return (int)hipGetLastError();
 }
