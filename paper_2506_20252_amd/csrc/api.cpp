@@ -332,12 +332,22 @@ void make_room(int device, size_t need) {
 // partial vector, but must hold one whole vector; the partial vector is the
 // piece's last vector, or, with `items`, each edge's takes one lane of work
 // items appended to the step.  Otherwise every piece must be whole vectors.
-// False when the sizes rule the width out.
+// False when the sizes rule the width out.  With out == nullptr, only that
+// check (in O(1)).
 bool build_steps(const pat::PlanDesc& d, int in_bytes, int tile, int pack_tile, bool partial, bool items,
                  std::vector<pat::DevStep>* out) {
-  out->clear();
   const int64_t per_vec = in_bytes / d.esize_in;  // elements per vector
   if (per_vec < 1) return false;
+  if (!out) {
+    // Only whether the width is possible: every piece but the last has the
+    // first one's length, so those two decide.
+    for (int piece : {0, d.pieces - 1}) {
+      const int64_t len = std::min<int64_t>(d.piece_elems, d.count - int64_t(piece) * d.piece_elems);
+      if (partial ? len < per_vec : (len * d.esize_in) % in_bytes != 0) return false;
+    }
+    return true;
+  }
+  out->clear();
   for (int piece = 0; piece < d.pieces; ++piece) {
     const int64_t e0 = int64_t(piece) * d.piece_elems;
     const int64_t len = std::min<int64_t>(d.piece_elems, d.count - e0);
@@ -1180,9 +1190,8 @@ pat_status_t pat_plan_info(pat_collective_t coll, int nranks, size_t count, pat_
   bool has[3] = {true, false, false};
   for (int path = 1; path < 3; ++path) {
     const pat::Variant v = variant_for((int)coll, dtype, path);
-    std::vector<pat::DevStep> steps;
     has[path] = build_steps(d, pat::variant_in_bytes(v), pat::variant_tile(v), pat::variant_pack_tile(v),
-                            path == 2 && pat::variant_partial(v), pat::variant_partial_items(v), &steps);
+                            path == 2 && pat::variant_partial(v), pat::variant_partial_items(v), nullptr);
   }
   info.vector_path = aligned_path(has);
   info.count = count;

@@ -417,12 +417,10 @@ double step_bytes(const PlanDesc& d, int s, int64_t elems) {
 double algorithmic_bytes(const PlanDesc& d) {
   if (d.count == 0) return 0.0;
   if (d.N == 1) return 2.0 * double(d.count) * d.esize_in;  // a copy
+  // Every piece runs every step, and step_bytes is linear in the piece's
+  // length, whose sum over the pieces is `count`.
   double total = 0.0;
-  for (int piece = 0; piece < d.pieces; ++piece) {
-    const int64_t e0 = int64_t(piece) * d.piece_elems;
-    const int64_t len = std::min<int64_t>(d.piece_elems, d.count - e0);
-    for (int s = 0; s < (int)d.exec.size(); ++s) total += step_bytes(d, s, len);
-  }
+  for (int s = 0; s < (int)d.exec.size(); ++s) total += step_bytes(d, s, d.count);
   return total;
 }
 
