@@ -691,11 +691,35 @@ pat::KCtx make_ctx(const HostPlan& h, int vi, const void* const* d_send, void* c
 }
 
 // The fused range of a call (stream and graph modes).
+// The fused launch of a plan, with the steps whose edges it caches: the
+// longest run of its narrow end (the all-gather's first steps, the
+// reduce-scatter's last) holding at most pat::kTreeCacheEdges entries in
+// pat::kTreeCacheSteps steps, whose entries follow each other in the table.
+// PAT_TREE_EDGE_CACHE=0 turns the cache off.
 pat::TreeRange tree_range(const HostPlan& h, int vi) {
   pat::TreeRange tr{};
   const auto& steps = h.steps[vi];
   fused_range(h.desc, steps.empty() ? 0 : steps[0].V, fusion_now(), &tr.s0, &tr.s1, &tr.tile_vecs);
-  if (tr.s1 > tr.s0) tr.tiles = (steps[0].V + tr.tile_vecs - 1) / tr.tile_vecs;
+  if (tr.s1 <= tr.s0) return tr;
+  tr.tiles = (steps[0].V + tr.tile_vecs - 1) / tr.tile_vecs;
+  const char* e = std::getenv("PAT_TREE_EDGE_CACHE");
+  if (e && std::atoi(e) == 0) return tr;
+  auto fits = [&](int s) { return tr.c1 - tr.c0 < pat::kTreeCacheSteps && tr.cn + steps[s].k <= pat::kTreeCacheEdges; };
+  tr.c0 = tr.c1 = h.desc.coll == 0 ? tr.s0 : tr.s1;
+  if (h.desc.coll == 0)
+    while (tr.c1 < tr.s1 && fits(tr.c1)) tr.cn += steps[tr.c1++].k;
+  else
+    while (tr.c0 > tr.s0 && fits(tr.c0 - 1)) tr.cn += steps[--tr.c0].k;
+  if (tr.cn == 0) return tr;
+  tr.ce0 = steps[tr.c0].entry0;
+  for (int s = tr.c0, end = 0; s < tr.c1; ++s) {
+    if (steps[s].entry0 != tr.ce0 + end) {  // not one run of the table: no cache
+      tr.c0 = tr.c1 = tr.cn = tr.ce0 = 0;
+      return tr;
+    }
+    end += steps[s].k;
+    tr.cend[s - tr.c0] = (int16_t)end;
+  }
   return tr;
 }
 

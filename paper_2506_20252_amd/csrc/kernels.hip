@@ -202,9 +202,13 @@ static_assert(kTreeThreads % 64 == 0 && kTreeThreads <= 1024, "tree workgroup: w
 
 // One step of one tree in a fused range: the pairs (entry i, vector v)
 // with i < k and v in [t0, t0 + TV), flattened vector-fastest so that lanes
-// sweep each edge's tile contiguously, U pairs per lane at a time.
-template <class Op>
-__device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV) {
+// sweep each edge's tile contiguously, U pairs per lane at a time.  CACHED:
+// the step's edges were resolved for this tree at the start of the launch and
+// sit in LDS at `cached`, so a lane reads its edges there instead of loading
+// the entries and pointer tables, and a narrow step is one data round trip.
+template <class Op, bool CACHED>
+__device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV,
+                                               const typename Op::Edge* cached) {
   constexpr int U = Op::U;
   const int64_t n = (int64_t)st.k * TV;
   for (int64_t base = 0; base < n; base += (int64_t)kTreeThreads * U) {
@@ -222,7 +226,7 @@ __device__ __forceinline__ void tree_step_impl(const KCtx& cx, const DevStep& st
         vv[j] = t0 + (f - i * TV);
       }
     }
-    Op::template batch<true>(cx, st, rr, ii, vv);
+    Op::template batch<true, CACHED>(cx, st, rr, ii, vv, cached);
   }
 }
 
@@ -369,31 +373,46 @@ struct AgOp {
   // vv[j] < 0 marks an unused slot.  In phases (entries, then pointer tables,
   // then data), so that each level of dependent loads is in flight for all U
   // vectors at once.
-  template <bool TREE>
+  // CACHED: the edges of entries ii[] are at cached[ii[j]] (LDS).
+  template <bool TREE, bool CACHED = false>
   __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
-                               const int64_t (&vv)[U]) {
-    Unit x[U];
+                               const int64_t (&vv)[U], const Edge* cached = nullptr) {
     Edge e[U];
-    DevEntry en[U];
+    if constexpr (CACHED) {
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) e[j] = cached[ii[j]];
+    } else {
+      DevEntry en[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
+    }
+    move(cx, st, [&](int j) -> const Edge& { return e[j]; }, vv);
+  }
+
+  // The data phase of a batch: U vectors per lane; e(j) is pair j's edge.
+  template <class E>
+  __device__ __forceinline__ static void move(const KCtx& cx, const DevStep& st, E e, const int64_t (&vv)[U]) {
+    Unit x[U];
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
-#pragma unroll
-    for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
-#pragma unroll
-    for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) x[j] = ldg<Unit, NT, kA>(e[j].src + off(cx, st, vv[j]));
+      if (vv[j] >= 0) x[j] = ldg<Unit, NT, kA>(e(j).src + off(cx, st, vv[j]));
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) put(cx, st, e[j], vv[j], x[j]);
+      if (vv[j] >= 0) put(cx, st, e(j), vv[j], x[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk
-  // (a partial last vector among them).
-  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool) {
-    tree_step_impl<AgOp>(cx, st, c, t0, TV);
+  // (a partial last vector among them); `cached`: the step's resolved edges.
+  template <bool CACHED>
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool,
+                                   const Edge* cached) {
+    tree_step_impl<AgOp, CACHED>(cx, st, c, t0, TV, cached);
   }
 };
 
@@ -746,34 +765,47 @@ struct RsOp {
   // (entries, then pointer tables, then data), so that each level of
   // dependent loads is in flight for all U vectors at once; conversions come
   // after every load has been issued.
-  template <bool TREE>
+  // CACHED: the edges of entries ii[] are at cached[ii[j]] (LDS).
+  template <bool TREE, bool CACHED = false>
   __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
-                               const int64_t (&vv)[U]) {
+                               const int64_t (&vv)[U], const Edge* cached = nullptr) {
     Edge e[U];
-    DevEntry en[U];
+    if constexpr (CACHED) {
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) e[j] = cached[ii[j]];
+    } else {
+      DevEntry en[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
+    }
+    move(cx, st, [&](int j) -> const Edge& { return e[j]; }, vv);
+  }
+
+  // The data phase of a batch: U vectors per lane; e(j) is pair j's edge.
+  template <class E>
+  __device__ __forceinline__ static void move(const KCtx& cx, const DevStep& st, E e, const int64_t (&vv)[U]) {
     in_t ra[U], rb[U];
     acc_t xa[U], xb[U];
-#pragma unroll
-    for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) en[j] = cx.entries[st.entry0 + ii[j]];
-#pragma unroll
-    for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       if (vv[j] >= 0) {
         if constexpr (kSameVec) {
-          xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
-          xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
+          xa[j] = ldg<acc_t, NT, kA>(e(j).own + off<acc_t>(vv[j], st.V, st.back));
+          xb[j] = ldg<acc_t, NT, kA>(e(j).child + off<acc_t>(vv[j], st.V, st.back));
         } else {
-          if (e[j].own_in)
-            ra[j] = ldg<in_t, NT, kA>(e[j].own + off<in_t>(vv[j], st.V, st.back));
+          if (e(j).own_in)
+            ra[j] = ldg<in_t, NT, kA>(e(j).own + off<in_t>(vv[j], st.V, st.back));
           else
-            xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
-          if (e[j].child_in)
-            rb[j] = ldg<in_t, NT, kA>(e[j].child + off<in_t>(vv[j], st.V, st.back));
+            xa[j] = ldg<acc_t, NT, kA>(e(j).own + off<acc_t>(vv[j], st.V, st.back));
+          if (e(j).child_in)
+            rb[j] = ldg<in_t, NT, kA>(e(j).child + off<in_t>(vv[j], st.V, st.back));
           else
-            xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
+            xb[j] = ldg<acc_t, NT, kA>(e(j).child + off<acc_t>(vv[j], st.V, st.back));
         }
       }
     }
@@ -783,27 +815,33 @@ struct RsOp {
       if (vv[j] >= 0) {
         acc_t a = xa[j], b = xb[j];
         if constexpr (!kSameVec) {
-          if (e[j].own_in) a = R::widen(ra[j]);
-          if (e[j].child_in) b = R::widen(rb[j]);
+          if (e(j).own_in) a = R::widen(ra[j]);
+          if (e(j).child_in) b = R::widen(rb[j]);
         }
         sum[j] = R::add(a, b);
       }
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) store(e[j], vv[j], st.V, st.back, sum[j]);
+      if (vv[j] >= 0) store(e(j), vv[j], st.V, st.back, sum[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk;
   // with kItems the workgroup of the last tile also takes the edges' partial
   // vectors.
-  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool last) {
-    tree_step_impl<RsOp>(cx, st, c, t0, TV);
+  template <bool CACHED>
+  __device__ static void tree_step(const KCtx& cx, const DevStep& st, int c, int64_t t0, int64_t TV, bool last,
+                                   const Edge* cached) {
+    tree_step_impl<RsOp, CACHED>(cx, st, c, t0, TV, cached);
     if constexpr (kItems) {
       if (last && st.back) {
         for (int i = threadIdx.x; i < st.k; i += kTreeThreads) {
-          const DevEntry en = cx.entries[st.entry0 + i];
-          part(st, edge_of(cx, st, wrap_add(c, en.p, cx.N), en));
+          if constexpr (CACHED) {
+            part(st, cached[i]);
+          } else {
+            const DevEntry en = cx.entries[st.entry0 + i];
+            part(st, edge_of(cx, st, wrap_add(c, en.p, cx.N), en));
+          }
         }
       }
     }
@@ -866,17 +904,56 @@ __global__ __launch_bounds__(kThreads) void step2_kernel(KCtx cx, int ia, int ib
 // before the first step and after each step's barrier (the last step gets a
 // barrier of its own then), so that step k of this workgroup took
 // stamps[k + 1] - stamps[k] ticks.
+//
+// The edges of the launch-level steps [tr.c0, tr.c1) (tr.cn of them, at most
+// kTreeCacheEdges: the narrow end of the range) are resolved for this tree
+// once into LDS: their entries and pointer tables do not change during the
+// operation, so those steps then wait for one data round trip each instead
+// of a chain of three.  Lane t resolves entry t, its step found from the
+// kernel arguments, so the fill costs one chain of two loads; it runs at the
+// start when the cached steps come first (all-gather), else during the last
+// step before them (reduce-scatter), whose barrier then also covers it.
+template <class Op>
+__device__ __forceinline__ void fill_edge_cache(const KCtx& cx, const TreeRange& tr, int c,
+                                                typename Op::Edge* cache) {
+  for (int t = threadIdx.x; t < tr.cn; t += kTreeThreads) {
+    int s = tr.c0;
+#pragma unroll
+    for (int i = 0; i < kTreeCacheSteps - 1; ++i)
+      if (i < tr.c1 - tr.c0 - 1 && t >= tr.cend[i]) s = tr.c0 + i + 1;
+    const DevStep st = cx.steps[s];
+    const DevEntry en = cx.entries[tr.ce0 + t];
+    cache[t] = Op::edge_of(cx, st, wrap_add(c, en.p, cx.N), en);
+  }
+}
+
 template <class Op>
 __global__ __launch_bounds__(kTreeThreads) void tree_kernel(KCtx cx, TreeRange tr) {
+  __shared__ typename Op::Edge cache[kTreeCacheEdges];
   const int c = (int)(blockIdx.x / tr.tiles);
   const int64_t tile = (int64_t)blockIdx.x - (int64_t)c * tr.tiles;
   const int64_t t0 = tile * tr.tile_vecs;
   uint64_t* const stamp = cx.stamps ? cx.stamps + (int64_t)blockIdx.x * (tr.s1 - tr.s0 + 1) : nullptr;
   if (stamp && threadIdx.x == 0) stamp[0] = wall_clock64();
+  const bool cached = tr.cn > 0 && tr.cn <= kTreeCacheEdges && tr.c1 - tr.c0 <= kTreeCacheSteps &&
+                      tr.c0 >= tr.s0 && tr.c1 <= tr.s1 && tr.c0 < tr.c1;
+  if (cached && tr.c0 == tr.s0) {
+    fill_edge_cache<Op>(cx, tr, c, cache);
+    __syncthreads();
+  }
+  int coff = 0;  // first cached edge of the current step
   for (int s = tr.s0; s < tr.s1; ++s) {
     const DevStep st = cx.steps[s];
     const int64_t left = st.V - t0;
-    Op::tree_step(cx, st, c, t0, left < tr.tile_vecs ? left : tr.tile_vecs, tile == tr.tiles - 1);
+    const bool hit = cached && s >= tr.c0 && s < tr.c1;
+    const int64_t TV = left < tr.tile_vecs ? left : tr.tile_vecs;
+    if (hit) {
+      Op::template tree_step<true>(cx, st, c, t0, TV, tile == tr.tiles - 1, cache + coff);
+      coff += st.k;
+    } else {
+      Op::template tree_step<false>(cx, st, c, t0, TV, tile == tr.tiles - 1, nullptr);
+    }
+    if (cached && s + 1 == tr.c0) fill_edge_cache<Op>(cx, tr, c, cache);  // c0 > s0: the barrier follows
     if (s + 1 < tr.s1 || stamp) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();

@@ -95,10 +95,22 @@ hipError_t launch_step2(Variant v, bool streaming, int64_t grain, const KCtx& cx
                         const DevStep& b, hipStream_t stream);
 // Fused range: launch-level steps [s0, s1) of one piece, run by one
 // workgroup per (tree, tile of tile_vecs vectors); tiles = ceil(V / tile_vecs).
+// Most slot entries, and steps, whose edges a fused launch resolves into LDS.
+constexpr int kTreeCacheEdges = 128;
+constexpr int kTreeCacheSteps = 16;
+
 struct TreeRange {
   int32_t s0, s1;
   int64_t tile_vecs;
   int64_t tiles;
+  // Steps [c0, c1) within [s0, s1) whose edges each workgroup resolves into
+  // LDS once: their cn entries (at most kTreeCacheEdges; 0: none) are
+  // entries [ce0, ce0 + cn) of the plan, and entry ce0 + t belongs to step
+  // c0 + (the number of cend[] values <= t), cend[i] being the end of step
+  // c0 + i relative to ce0.
+  int32_t c0, c1;
+  int32_t cn, ce0;
+  int16_t cend[kTreeCacheSteps];
 };
 hipError_t launch_tree(Variant v, bool streaming, const KCtx& cx, const TreeRange& tr, hipStream_t stream);
 // Persistent execution: one launch of `grid` workgroups that take per-step
