@@ -695,7 +695,8 @@ pat::KCtx make_ctx(const HostPlan& h, int vi, const void* const* d_send, void* c
 // longest run of its narrow end (the all-gather's first steps, the
 // reduce-scatter's last) holding at most pat::kTreeCacheEdges entries in
 // pat::kTreeCacheSteps steps, whose entries follow each other in the table.
-// PAT_TREE_EDGE_CACHE=0 turns the cache off.
+// PAT_TREE_EDGE_CACHE=0 turns the cache off.  (Leaving the all-gather's first
+// step out, to fill during it, measured 0.3 us slower on MI355X.)
 pat::TreeRange tree_range(const HostPlan& h, int vi) {
   pat::TreeRange tr{};
   const auto& steps = h.steps[vi];
@@ -710,7 +711,10 @@ pat::TreeRange tree_range(const HostPlan& h, int vi) {
     while (tr.c1 < tr.s1 && fits(tr.c1)) tr.cn += steps[tr.c1++].k;
   else
     while (tr.c0 > tr.s0 && fits(tr.c0 - 1)) tr.cn += steps[--tr.c0].k;
-  if (tr.cn == 0) return tr;
+  if (tr.cn == 0) {
+    tr.c0 = tr.c1 = 0;
+    return tr;
+  }
   tr.ce0 = steps[tr.c0].entry0;
   for (int s = tr.c0, end = 0; s < tr.c1; ++s) {
     if (steps[s].entry0 != tr.ce0 + end) {  // not one run of the table: no cache
