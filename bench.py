@@ -823,6 +823,10 @@ def main():
                 "timing": "operation time / launches (no per-launch trace in this mode)"}
     achieved = roof.pop("achieved")
     traffic = committed_traffic(args.workload, args.mode, roof["kernel"])
+    if traffic is not None and roof.get("avg_launch_us"):
+        # the counted HBM-side bytes over the same launch time: how busy HBM
+        # itself was (below `frac` where the kernel hits in cache)
+        roof["traffic_frac"] = round(traffic / (roof["avg_launch_us"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
 
     out = {
         "metric": METRIC,
