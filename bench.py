@@ -291,10 +291,10 @@ def other_workloads(reps=50):
 def streaming_ceiling(nbytes=4 << 30, reps=10):
     """The GPU's streaming bandwidth for the step kernels' access shapes, from
     the plain probe kernels of libpatceiling.so (one 16-byte vector per lane,
-    nontemporal): a copy (an all-gather step into leaves), a copy into two
-    buffers (an all-gather step into forwarding receivers), and a float32 add
-    of two buffers into a third (the reduce-scatter shape).  GB/s of bytes
-    read + written."""
+    nontemporal): a read-only and a write-only stream, a copy (an all-gather
+    step into leaves), a copy into two buffers (an all-gather step into
+    forwarding receivers), and a float32 add of two buffers into a third (the
+    reduce-scatter shape).  GB/s of bytes read + written."""
     import ctypes
 
     import torch
@@ -303,18 +303,25 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built: run __graft_entry__.build()")
     lib = ctypes.CDLL(path)
-    for name, nargs in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3)):
+    for name, nargs in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3),
+                        ("pat_ceiling_read", 2)):
         fn = getattr(lib, name)
         fn.argtypes = [ctypes.c_void_p] * nargs + [ctypes.c_size_t, ctypes.c_void_p]
         fn.restype = ctypes.c_int
+    lib.pat_ceiling_write.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32, ctypes.c_void_p]
+    lib.pat_ceiling_write.restype = ctypes.c_int
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     a = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
     b = torch.full_like(a, 2.0)
     c = torch.empty_like(a)
+    sink = torch.zeros(1024, dtype=torch.int32, device=dev)
     out = {"bytes_per_buffer": nbytes, "kernel": "16 B/lane, 256 lanes/workgroup, nontemporal"}
-    # the two-buffer copy runs last: it overwrites b, an input of the add
-    runs = (("copy_gbps", 2, lambda: lib.pat_ceiling_copy(a.data_ptr(), c.data_ptr(), nbytes, stream.cuda_stream)),
+    # the two-buffer copy runs last: it overwrites b, an input of the add;
+    # the write-only stream fills c before the copy overwrites it
+    runs = (("read_gbps", 1, lambda: lib.pat_ceiling_read(a.data_ptr(), sink.data_ptr(), nbytes, stream.cuda_stream)),
+            ("write_gbps", 1, lambda: lib.pat_ceiling_write(c.data_ptr(), nbytes, 0x40400000, stream.cuda_stream)),
+            ("copy_gbps", 2, lambda: lib.pat_ceiling_copy(a.data_ptr(), c.data_ptr(), nbytes, stream.cuda_stream)),
             ("rs_shape_gbps", 3, lambda: lib.pat_ceiling_add(a.data_ptr(), b.data_ptr(), c.data_ptr(), nbytes,
                                                              stream.cuda_stream)),
             ("ag_shape_gbps", 3, lambda: lib.pat_ceiling_copy2(a.data_ptr(), c.data_ptr(), b.data_ptr(), nbytes,
@@ -333,9 +340,13 @@ def streaming_ceiling(nbytes=4 << 30, reps=10):
         out[key] = round(streams * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
         if key == "rs_shape_gbps" and not bool(torch.equal(c[:1 << 20], torch.full_like(c[:1 << 20], 3.0))):
             raise RuntimeError("ceiling probe: wrong sum")
+        if key == "write_gbps" and not bool(torch.equal(c[-(1 << 20):], torch.full_like(c[-(1 << 20):], 3.0))):
+            raise RuntimeError("ceiling probe: wrong fill")  # 0x40400000 is float32 3.0
+        if key == "read_gbps" and bool(sink.any()):
+            raise RuntimeError("ceiling probe: the read found a pattern its input does not hold")
     if not (bool(torch.equal(b[:1 << 20], a[:1 << 20])) and bool(torch.equal(c[:1 << 20], a[:1 << 20]))):
         raise RuntimeError("ceiling probe: wrong two-buffer copy")
-    del a, b, c
+    del a, b, c, sink
     torch.cuda.empty_cache()
     return out
 

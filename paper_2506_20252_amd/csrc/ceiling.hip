@@ -3,7 +3,8 @@
 // shape of an all-gather step into leaves), a copy into two buffers (one
 // read, two writes, the shape of an all-gather step into forwarding
 // receivers) and a float32 add of two streams into a third (two reads, one
-// write, the shape of a reduce-scatter step).  One 16-byte vector per lane, 256 lanes per
+// write, the shape of a reduce-scatter step); and a read-only and a
+// write-only stream, the two ends of that mix.  One 16-byte vector per lane, 256 lanes per
 // workgroup, nontemporal loads and stores: the fastest form of each on
 // MI355X among 1, 2, 4 and 8 vectors per lane.  Not part of the collectives.
 #include <hip/hip_runtime.h>
@@ -43,6 +44,22 @@ __global__ __launch_bounds__(kThreads) void add_kernel(const v4f* a, const v4f* 
     const v4f y = __builtin_nontemporal_load((const PAT_GLOBAL v4f*)(b + i));
     __builtin_nontemporal_store(x + y, (PAT_GLOBAL v4f*)(c + i));
   }
+}
+
+// Read-only and write-only streams: the two ends of the mix the step
+// kernels run.  The read folds each lane's vector into a value that is
+// stored only if it equals a pattern no probe input holds, so the loads stay.
+__global__ __launch_bounds__(kThreads) void read_kernel(const v4u* src, v4u* sink, int64_t n, v4u never) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) {
+    const v4u x = __builtin_nontemporal_load((const PAT_GLOBAL v4u*)(src + i));
+    if (x.x == never.x && x.y == never.y && x.z == never.z && x.w == never.w) sink[threadIdx.x] = x;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void write_kernel(v4u* dst, int64_t n, v4u value) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) __builtin_nontemporal_store(value, (PAT_GLOBAL v4u*)(dst + i));
 }
 
 // Chunk copies at a skew: chunk c (16 vectors of 16 bytes) of the chunks with
@@ -101,6 +118,30 @@ extern "C" int pat_ceiling_add(const void* a, const void* b, void* c, size_t byt
   if (int e = launch_check(n)) return e;
   hipLaunchKernelGGL(add_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
                      (const v4f*)a, (const v4f*)b, (v4f*)c, n);
+  return (int)hipGetLastError();
+}
+
+// Reads src[0 .. bytes); `sink` (16-byte aligned, 4096 bytes) is written only
+// if some 16-byte vector of src equals {1, 2, 3, 4} (words).  Same rules as
+// the copy.
+extern "C" int pat_ceiling_read(const void* src, void* sink, size_t bytes, hipStream_t stream) {
+  if (!src || !sink || bytes % 16 || ((uintptr_t)src | (uintptr_t)sink) % 16) return (int)hipErrorInvalidValue;
+  const int64_t n = (int64_t)(bytes / 16);
+  if (int e = launch_check(n)) return e;
+  const v4u never = {1u, 2u, 3u, 4u};
+  hipLaunchKernelGGL(read_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
+                     (const v4u*)src, (v4u*)sink, n, never);
+  return (int)hipGetLastError();
+}
+
+// dst[0 .. bytes) = the word `value`, repeated; same rules as the copy.
+extern "C" int pat_ceiling_write(void* dst, size_t bytes, uint32_t value, hipStream_t stream) {
+  if (!dst || bytes % 16 || (uintptr_t)dst % 16) return (int)hipErrorInvalidValue;
+  const int64_t n = (int64_t)(bytes / 16);
+  if (int e = launch_check(n)) return e;
+  const v4u v = {value, value, value, value};
+  hipLaunchKernelGGL(write_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream,
+                     (v4u*)dst, n, v);
   return (int)hipGetLastError();
 }
 

@@ -116,11 +116,12 @@ def test_plan_info_workloads():
 
 def test_ceiling_probe_library_exports_and_checks_arguments():
     """The benchmark's streaming-ceiling probes (not part of the collectives)
-    load, export their three entry points, and refuse null or misaligned
-    buffers and sizes that are not whole 16-byte vectors before any launch."""
+    load, export their entry points, and refuse null or misaligned buffers and
+    sizes that are not whole 16-byte vectors before any launch."""
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2506_20252_amd", "libpatceiling.so"))
     invalid = 1  # hipErrorInvalidValue
-    for name, nbuf in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3)):
+    for name, nbuf in (("pat_ceiling_copy", 2), ("pat_ceiling_copy2", 3), ("pat_ceiling_add", 3),
+                       ("pat_ceiling_read", 2)):
         fn = getattr(lib, name)
         fn.argtypes = [ctypes.c_void_p] * nbuf + [ctypes.c_size_t, ctypes.c_void_p]
         fn.restype = ctypes.c_int
@@ -128,6 +129,12 @@ def test_ceiling_probe_library_exports_and_checks_arguments():
         assert fn(*([None] + good[1:]), 4096, None) == invalid, name
         assert fn(*(good[:-1] + [good[-1] + 8]), 4096, None) == invalid, name
         assert fn(*good, 4100, None) == invalid, name
+    fn = lib.pat_ceiling_write
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    assert fn(None, 4096, 0, None) == invalid
+    assert fn(0x100008, 4096, 0, None) == invalid
+    assert fn(0x100000, 4100, 0, None) == invalid
 
 
 def test_tensor_wrappers_check_shapes_and_dtypes_before_any_call():
