@@ -55,13 +55,15 @@
 // stores stream (nontemporal) and the work-item order are launch arguments,
 // chosen per plan.
 //
-// The all-gather's stores into receive buffers stream (nontemporal) even
-// where the plan keeps its accesses cached: the operation never reads them
-// again, and caching them only evicts the slots the next steps read
-// (measured on MI355X: all-gathers of N=1000 ranks with 256 B chunks and of
-// N=24 with 64 KiB chunks run 9-10% faster).  The reduce-scatter's raw
-// inputs, also read once, measured no different streamed and keep the plan's
-// policy.
+// The all-gather's whole-vector stores into receive buffers stream
+// (nontemporal) even where the plan keeps its accesses cached: the operation
+// never reads them again, and caching them only evicts the slots the next
+// steps read (measured on MI355X: all-gathers of N=1000 ranks with 256 B
+// chunks and of N=24 with 64 KiB chunks run 9-10% faster).  A chunk's partial
+// last vector, a few element stores into a line shared with the next chunk,
+// keeps the plan's policy: streamed, it made an odd count 38% slower.  The
+// reduce-scatter's raw inputs, also read once, measured no different
+// streamed and keep the plan's policy.
 #ifndef PAT_UNROLL
 #define PAT_UNROLL 2
 #endif
@@ -253,7 +255,7 @@ struct AgOp {
   static constexpr int kTile = kThreads * TU;      // vectors of one tiled work item
   static constexpr int kPackTile = kThreads * U;   // vectors of one packed work item
   static constexpr bool kTail = kA > 0;
-  static constexpr bool RNT = true;  // stores into receive buffers: always streaming
+  static constexpr bool RNT = true;  // whole-vector stores into receive buffers: always streaming
   static_assert(!kTail || sizeof(Unit) == 16, "relaxed all-gather moves 16-byte vectors");
 
   struct Edge {
@@ -302,13 +304,13 @@ struct AgOp {
     if constexpr (kTail) {
       if (st.back && v == st.V - 1) {
         if (cx.esize == 4) {
-          stg_from<RNT, 4>(e.dst + o, x, st.back);
+          stg_from<NT, 4>(e.dst + o, x, st.back);
           if (e.dst2) stg_from<NT, 4>(e.dst2 + o, x, st.back);
-          if (e.dst3) stg_from<RNT, 4>(e.dst3 + o, x, st.back);
+          if (e.dst3) stg_from<NT, 4>(e.dst3 + o, x, st.back);
         } else {
-          stg_from<RNT, 2>(e.dst + o, x, st.back);
+          stg_from<NT, 2>(e.dst + o, x, st.back);
           if (e.dst2) stg_from<NT, 2>(e.dst2 + o, x, st.back);
-          if (e.dst3) stg_from<RNT, 2>(e.dst3 + o, x, st.back);
+          if (e.dst3) stg_from<NT, 2>(e.dst3 + o, x, st.back);
         }
         return;
       }

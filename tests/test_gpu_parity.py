@@ -660,6 +660,26 @@ def test_top_fusion_is_bit_identical_to_step_kernels(n, count, dtype):
     compare_rs_full({"off": outs["off"][1]}, n, count, dtype, DIST[dtype], seed + 1)
 
 
+@pytest.mark.parametrize("n,count,dtype", [(1000, 64, "float32"), (24, 32768, "bfloat16"), (6, 1024, "int32"),
+                                           (37, 1001, "bfloat16"), (129, 300, "float32")])
+def test_tree_edge_cache_is_bit_identical(n, count, dtype, monkeypatch):
+    """The fused launch's LDS edge cache (on by default; PAT_TREE_EDGE_CACHE=0
+    turns it off) changes where lanes find their edges, not what they move:
+    the same bits with and without it, for both collectives, and the
+    oracle's."""
+    seed = 0xEC0 + n
+    outs = {}
+    for flag in ("0", "1"):
+        monkeypatch.setenv("PAT_TREE_EDGE_CACHE", flag)
+        ag, host_in = run_ag(n, count, dtype, seed, mode="stream")
+        rs = run_rs(n, count, dtype, seed + 1, mode="stream")
+        outs[flag] = (ag, rs)
+    np.testing.assert_array_equal(outs["1"][0], outs["0"][0])
+    np.testing.assert_array_equal(outs["1"][1], outs["0"][1])
+    np.testing.assert_array_equal(outs["1"][0], D.allgather(host_in))
+    compare_rs_full({"cache": outs["1"][1]}, n, count, dtype, DIST[dtype], seed + 1)
+
+
 def _max_chunks(n, t):
     return max(len(P) for _, P in opat.schedule(n, t))
 
