@@ -388,8 +388,53 @@ def misalign_probe(chunks=500000, reps=20):
                          "gbps_read_plus_write": round(2 * chunks * 256 / (us * 1e-6) / 1e9, 1)})
     if not bool(torch.equal(dst[4:4 + chunks * 256], src[4:4 + chunks * 256])):
         raise RuntimeError("chunk copy probe: wrong copy")
+    del src, dst
+    torch.cuda.empty_cache()
     print(json.dumps({"metric": "256-byte chunk copies at a skew (why misaligned all-gathers cost more)",
-                      "chunks": chunks, "rows": rows}), flush=True)
+                      "chunks": chunks, "rows": rows, "allgather": misaligned_allgather()}), flush=True)
+
+
+def misaligned_allgather(n=1000, reps=50):
+    """The all-gather of workload 6's shape (N=1000, float32) with every row
+    16-byte aligned (64 elements), every row one element off a 16-byte
+    boundary (64 elements), and an odd count (63 elements): microseconds per
+    operation (median of 5 runs of `reps`), each result checked on 4 rows."""
+    import torch
+
+    import synth
+    from paper_2506_20252_amd import pat
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    out = []
+    for label, count, skew in (("aligned", 64, 0), ("one element off", 64, 1), ("odd count", 63, 0)):
+        sstride, rstride = count + skew, n * count + skew
+        sflat = torch.empty(n * sstride + skew, dtype=torch.float32, device=dev)
+        rflat = torch.empty(n * rstride + skew, dtype=torch.float32, device=dev)
+        send = [sflat[skew + r * sstride: skew + r * sstride + count] for r in range(n)]
+        recv = [rflat[skew + r * rstride: skew + r * rstride + n * count] for r in range(n)]
+        for x in range(n):
+            synth.fill(send[x], "f32_pm1", 0x5041544, x)
+        S, R = pat.pointer_array(send), pat.pointer_array(recv)
+        for _ in range(3):
+            pat.check(pat.pat_allgather(S, R, count, "float32", n, stream))
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(reps):
+                pat.check(pat.pat_allgather(S, R, count, "float32", n, stream))
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3 / reps)
+        host = torch.stack([x.cpu() for x in send])
+        if not all(torch.equal(recv[r].cpu().view(n, count), host) for r in (0, 1, n // 2, n - 1)):
+            raise RuntimeError(f"misaligned all-gather probe ({label}): wrong result")
+        out.append({"case": label, "count": count, "row_offset_elems": skew, "us": round(statistics.median(ts), 1)})
+        del send, recv, S, R, sflat, rflat
+        torch.cuda.empty_cache()
+    return out
 
 
 def budget_sweep(wid, reps, max_slot_bytes=32 << 30, aggregation="pow2"):
