@@ -16,10 +16,11 @@ Prints one JSON line:
                 the timed region; against the 8 TB/s HBM3E peak; traffic from
                 the committed rocprofv3 counter summary when it matches the
                 current kernel source
-* cpu_baseline -- the CPU oracle timed in the same process: for reduce-scatter
-                the threaded C++ oracle (PAT association and fp64 plain sum)
-                over the whole operation on every host CPU, inputs regenerated
-                from the seed; in the same unit
+* cpu_baseline -- the CPU oracle timed in the same process: the threaded C++
+                oracle over the whole operation on every host CPU, inputs
+                regenerated from the seed (reduce-scatter: PAT association and
+                fp64 plain sum; all-gather: concatenation, repeated for at least
+                --cpu-seconds); in the same unit
 
 python bench.py [--steps K] [--warmup W] [--mode persistent|graph|stream]
                 [--workload 1..7] [--cpu-seconds S] [--no-cpu-baseline]
@@ -160,30 +161,43 @@ def cpu_baseline_rs(wid):
             "seconds": round(elapsed, 2)}
 
 
-def cpu_baseline_ag(wid, target_seconds, sample_inputs, m_cap):
-    """All-gather: the oracle's definition (concatenation, numpy, one thread)
-    on a bounded sample: every (receiver, chunk) pair, the first m elements of
-    each chunk, m calibrated so the run takes about `target_seconds`."""
-    from oracle import definitions as D
+def cpu_baseline_ag(wid, min_seconds=1.0):
+    """All-gather: the threaded C++ oracle over the whole operation -- every
+    receiver's row, the concatenation of the N send buffers regenerated from
+    the seed -- on every CPU this process may use, in blocks of receivers that
+    keep the host buffer under 256 MiB; repeated until at least `min_seconds`
+    have passed (small operations take milliseconds)."""
+    import numpy as np
+
+    from oracle import native
 
     coll, n, count, dtype, dist, seed, _ = WORKLOADS[wid]
     esize = 2 if dtype == "bfloat16" else 4
-
-    def run(x):
-        t0 = time.perf_counter()
-        D.allgather(x)
-        return time.perf_counter() - t0
-
-    m = min(count, m_cap, 2048)
-    elapsed = run(sample_inputs(m))
-    while elapsed < 0.6 * target_seconds and m < min(count, m_cap):
-        m = int(min(count, m_cap, max(2 * m, m * target_seconds / max(elapsed, 1e-3))))
-        elapsed = run(sample_inputs(m))
-    bus_bytes = float(n) * (n - 1) * m * esize
-    return {"value": round(bus_bytes / elapsed / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    block = max(1, (256 << 20) // max(1, n * count * esize))
+    np_dtype = {"int32": np.int32, "float32": np.float32, "bfloat16": np.uint16}[dtype]
+    buf = np.empty((min(block, n), n * count), dtype=np_dtype)
+    native.allgather(dtype, n, 1, dist=dist, seed=seed)  # load the library and the table first
+    used, reps = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        # receiver 0's row, from the generator, is the send buffers: the other
+        # blocks copy from it instead of generating them again
+        row0, used = native.allgather(dtype, n, count, dist=dist, seed=seed, r0=0, r1=1, out=buf[:1])
+        inputs = row0.reshape(n, count).copy()
+        for r0 in range(1, n, block):
+            r1 = min(n, r0 + block)
+            _, u = native.allgather(dtype, n, count, inputs=inputs, r0=r0, r1=r1, out=buf[:r1 - r0])
+            used = max(used, u)
+        reps += 1
+        elapsed = time.perf_counter() - t0
+        if elapsed >= min_seconds:
+            break
+    bus_bytes = float(n) * (n - 1) * count * esize * reps
+    return {"value": round(bus_bytes / elapsed / 1e9, 3), "unit": "GB/s", "cores": used, "kind": "oracle",
             "cpu_model": _cpu_model(), "host_cpus_visible": os.cpu_count(),
-            "sample": f"all {n} x {n} (receiver, chunk) pairs x the first {m} of {count} elements "
-                      f"({m / count:.3g} of the operation); numpy definition, one thread; {elapsed:.1f} s",
+            "sample": f"whole operation x {reps}: all {n} receivers x all {n} chunks of {count} elements, the send "
+                      f"buffers regenerated from the seed; concatenation; C++ std::thread oracle on {used} threads; "
+                      f"{elapsed:.2f} s",
             "seconds": round(elapsed, 2)}
 
 
@@ -785,7 +799,8 @@ def main():
                          "the calibration kernel for the memory-traffic counters)")
     ap.add_argument("--copy-probe-kind", default="torch", choices=["torch", "nt"])
     ap.add_argument("--workload", type=int, default=5, choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=1.0,
+                    help="all-gather CPU baseline: repeat the whole operation for at least this long")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true", help="skip the small-size latency figures")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the streaming-ceiling probes")
@@ -920,18 +935,7 @@ def main():
         if coll == "rs":
             out["cpu_baseline"] = cpu_baseline_rs(args.workload)
         else:
-            # The oracle's inputs: the first m positions of every chunk of the
-            # generator-filled send buffers (the collective only reads them).
-            import numpy as np
-
-            def sample_inputs(m):
-                part = send[..., :m].contiguous()
-                if dtype == "bfloat16":
-                    return part.view(torch.int16).cpu().numpy().view(np.uint16)
-                return part.cpu().numpy()
-
-            out["cpu_baseline"] = cpu_baseline_ag(args.workload, args.cpu_seconds, sample_inputs,
-                                                  min(count, 1 << 20))
+            out["cpu_baseline"] = cpu_baseline_ag(args.workload, args.cpu_seconds)
     del send, recv, sends, recvs
     torch.cuda.empty_cache()
     if not args.no_ceiling:

@@ -17,7 +17,8 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "-pthread", "-ffp-contract=off
 
 def build(verbose=False):
     tmp = LIB_PATH + ".tmp"
-    cmd = ["g++", *FLAGS, "-I", ROOT, os.path.join(HERE, "rs_oracle.cpp"), "-o", tmp]
+    cmd = ["g++", *FLAGS, "-I", ROOT, os.path.join(HERE, "rs_oracle.cpp"), os.path.join(HERE, "ag_oracle.cpp"),
+           "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"oracle build failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

@@ -1,5 +1,6 @@
-"""Pins for the threaded C++ oracle (oracle/rs_oracle.cpp): it must agree with
-the Python oracle, which the pins in test_oracle_pins.py tie to the paper.
+"""Pins for the threaded C++ oracle (oracle/rs_oracle.cpp, oracle/ag_oracle.cpp):
+it must agree with the Python oracle, which the pins in test_oracle_pins.py tie
+to the paper.
 
 * PAT association: bit-exact against the step-by-step executor
   (oracle.pat.reducescatter, a different construction: explicit steps and
@@ -9,7 +10,11 @@ the Python oracle, which the pins in test_oracle_pins.py tie to the paper.
 * regenerated inputs: equal to the array path fed with the host twin of the
   generator;
 * results do not depend on the thread count or on the destination range;
-* bf16 rounding ties go to even.
+* bf16 rounding ties go to even;
+* all-gather: every receiver's row is the concatenation of the send buffers
+  (oracle.definitions.allgather, and the Bruck / PAT step executors through
+  it), from arrays and from regenerated inputs, for any receiver range and
+  thread count.
 Nothing here calls the HIP library.
 """
 
@@ -96,3 +101,36 @@ def test_invalid_arguments_are_refused():
         native.reducescatter("float32", 4, 3, inputs=np.zeros((4, 4, 2), np.float32))
     with pytest.raises(ValueError):
         native.reducescatter("float32", 4, 3, dist="f32_normal", r0=2, r1=9)
+
+
+@pytest.mark.parametrize("dist,dtype", [("int32_pm2p20", "int32"), ("f32_normal", "float32"),
+                                        ("bf16_normal", "bfloat16")])
+@pytest.mark.parametrize("n,count", [(1, 5), (2, 1), (7, 13), (24, 33), (100, 3)])
+def test_allgather_is_the_definition(n, count, dist, dtype):
+    seed = 0xA6 + n
+    host = np.stack([synth.host_buffer(dist, seed, x, count) for x in range(n)])
+    exp = D.allgather(host).reshape(n, n * count)
+    got, _ = native.allgather(dtype, n, count, dist=dist, seed=seed)
+    assert (got == exp).all()
+    arr, _ = native.allgather(dtype, n, count, inputs=host)
+    assert (arr == exp).all()
+    # and the step executors of the schedule reach the same rows
+    ex, _ = pat.allgather(host, max(pat.ceil_log2(n) - 1, 0))
+    assert (np.asarray(ex).reshape(n, n * count) == exp).all()
+
+
+def test_allgather_ranges_threads_and_zero_count():
+    n, count, seed = 33, 1000, 0xA6A6
+    full, used = native.allgather("float32", n, count, dist="f32_normal", seed=seed)
+    assert used >= 1
+    one, used1 = native.allgather("float32", n, count, dist="f32_normal", seed=seed, nthreads=1)
+    assert used1 == 1 and (one.view(np.uint32) == full.view(np.uint32)).all()
+    buf = np.empty((7, n * count), dtype=np.float32)
+    part, _ = native.allgather("float32", n, count, dist="f32_normal", seed=seed, r0=20, r1=27, nthreads=3, out=buf)
+    assert part is buf and (part.view(np.uint32) == full[20:27].view(np.uint32)).all()
+    empty, _ = native.allgather("bfloat16", 5, 0, dist="bf16_normal", seed=1)
+    assert empty.shape == (5, 0)
+    with pytest.raises(ValueError):
+        native.allgather("float32", 4, 3, inputs=np.zeros((4, 2), np.float32))
+    with pytest.raises(ValueError):
+        native.allgather("float32", 4, 3, dist="f32_normal", r0=2, r1=9)
