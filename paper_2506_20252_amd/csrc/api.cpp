@@ -808,21 +808,20 @@ hipError_t enqueue_stream(const HostPlan& h, int coll, pat_dtype_t dt, int vi, c
       if (e != hipSuccess) return e;
     }
     const int first = s;
-    double bytes = 0.0;
     hipError_t e;
     if (fuse && s == tr.s0) {
       e = pat::launch_tree(var, h.streaming, cx, tr, q);
-      for (int k = tr.s0; k < tr.s1; ++k) bytes += launch_bytes(h, vi, k);
       s = tr.s1 - 1;
     } else {
       e = pat::launch_step(var, h.streaming, xcd_grain(h.xcd_run), cx, steps[s], q);
-      bytes = launch_bytes(h, vi, s);
     }
     if (e != hipSuccess) return e;
     if (traced) {
       const int j = trace->used;
       e = hipEventRecord(trace->ev[2 * j + 1], q);
       if (e != hipSuccess) return e;
+      double bytes = 0.0;
+      for (int k = first; k <= s; ++k) bytes += launch_bytes(h, vi, k);
       trace->bytes[j] = bytes;
       trace->kind[j] = fuse && first == tr.s0 ? 1 : 0;
       trace->step[j] = first;
