@@ -12,8 +12,8 @@ Prints one JSON line:
                 bracketed by its own HIP events (the median is reported too)
 * roofline   -- the dominant kernel's own rate: the algorithmic bytes of its
                 launches / their durations, from a HIP event pair recorded on
-                the kernels' stream around every launch of a traced pass after
-                the timed region; against the 8 TB/s HBM3E peak; traffic from
+                the kernels' stream around every launch of the first three
+                timed operations; against the 8 TB/s HBM3E peak; traffic from
                 the committed rocprofv3 counter summary when it matches the
                 current kernel source
 * cpu_baseline -- the CPU oracle timed in the same process: the threaded C++
@@ -675,20 +675,14 @@ def kernel_name(coll, dtype, path, streaming, kind):
     return ("tree_kernel<" if kind == 1 else "step_kernel<") + op + ">"
 
 
-def kernel_roofline(op, info, coll, dtype, reps=3):
-    """The traced pass: `reps` operations with a HIP event pair around every
-    kernel launch, recorded by the library on the kernels' stream, and each
-    launch's algorithmic bytes from the plan's byte model.  The dominant kernel
-    is the one with the most traced time; its rate is its launches' bytes
-    over their summed durations."""
-    import torch
-
+def kernel_roofline(info, coll, dtype, reps):
+    """The launch trace of the first `reps` timed operations: a HIP event pair
+    around every kernel launch, recorded by the library on the kernels' stream
+    (armed before the timed region), and each launch's algorithmic bytes from
+    the plan's byte model.  The dominant kernel is the one with the most traced
+    time; its rate is its launches' bytes over their summed durations."""
     from paper_2506_20252_amd import pat
     launches = info["launches_per_op"]
-    pat.check(pat.pat_trace_start(reps * launches))
-    for _ in range(reps):
-        pat.check(op(), "traced")
-    torch.cuda.synchronize()
     st, rows = pat.pat_trace_read(reps * launches)
     pat.check(st, "pat_trace_read")
     if len(rows) != reps * launches:
@@ -722,7 +716,8 @@ def kernel_roofline(op, info, coll, dtype, reps=3):
                         "median": round(statistics.median(rates) / HBM_PEAK_GBPS, 4),
                         "max": round(rates[-1] / HBM_PEAK_GBPS, 4)},
         "traced_ops": reps,
-        "timing": "HIP event pair around each launch on the kernels' stream (library launch trace)",
+        "timing": f"HIP event pair around each launch of the first {reps} timed operations, on the kernels' "
+                  "stream (library launch trace)",
         "kernels": kinds,
     }
 
@@ -880,12 +875,20 @@ def main():
     torch.cuda.synchronize()
     pat.check(pat.pat_check_device_status(stream))
 
+    # The launch trace covers the first operations of the timed region: an
+    # event pair around each launch adds a few microseconds per launch, so
+    # tracing all of them would slow the timed operations measurably (1% on
+    # workload 5, 16% on workload 4); three traced operations of twenty cost
+    # the mean under 0.2% on workload 5.
+    traced = min(args.steps, 3, (1 << 20) // max(1, info["launches_per_op"]))
+    if args.mode == "stream":
+        pat.check(pat.pat_trace_start(traced * info["launches_per_op"]))
     ms, rep_ms = time_ops(op, stream, args.steps)
     pat.check(pat.pat_check_device_status(stream))
     sec = ms / 1e3
     bus_per_rank = info["bus_bytes_per_rank"]
     if args.mode == "stream":
-        roof = kernel_roofline(op, info, coll, dtype)
+        roof = kernel_roofline(info, coll, dtype, traced)
     else:
         # no per-launch trace in these modes: the operation's time spread over its launches
         launches = 1 if args.mode == "persistent" else info["launches_per_op"]
