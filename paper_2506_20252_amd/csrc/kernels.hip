@@ -388,6 +388,7 @@ struct AgOp {
   template <bool TREE, bool CACHED = false>
   __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
                                const int64_t (&vv)[U], const Edge* cached = nullptr) {
+    Unit x[U];
     Edge e[U];
     if constexpr (CACHED) {
 #pragma unroll
@@ -402,20 +403,13 @@ struct AgOp {
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
     }
-    move(cx, st, [&](int j) -> const Edge& { return e[j]; }, vv);
-  }
-
-  // The data phase of a batch: U vectors per lane; e(j) is pair j's edge.
-  template <class E>
-  __device__ __forceinline__ static void move(const KCtx& cx, const DevStep& st, E e, const int64_t (&vv)[U]) {
-    Unit x[U];
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) x[j] = ldg<Unit, NT, kA>(e(j).src + off(cx, st, vv[j]));
+      if (vv[j] >= 0) x[j] = ldg<Unit, NT, kA>(e[j].src + off(cx, st, vv[j]));
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) put(cx, st, e(j), vv[j], x[j]);
+      if (vv[j] >= 0) put(cx, st, e[j], vv[j], x[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk
@@ -781,6 +775,8 @@ struct RsOp {
   __device__ static void batch(const KCtx& cx, const DevStep& st, const int (&rr)[U], const int (&ii)[U],
                                const int64_t (&vv)[U], const Edge* cached = nullptr) {
     Edge e[U];
+    in_t ra[U], rb[U];
+    acc_t xa[U], xb[U];
     if constexpr (CACHED) {
 #pragma unroll
       for (int j = 0; j < U; ++j)
@@ -794,29 +790,21 @@ struct RsOp {
       for (int j = 0; j < U; ++j)
         if (vv[j] >= 0) e[j] = edge_of(cx, st, TREE ? wrap_add(rr[j], en[j].p, cx.N) : rr[j], en[j]);
     }
-    move(cx, st, [&](int j) -> const Edge& { return e[j]; }, vv);
-  }
-
-  // The data phase of a batch: U vectors per lane; e(j) is pair j's edge.
-  template <class E>
-  __device__ __forceinline__ static void move(const KCtx& cx, const DevStep& st, E e, const int64_t (&vv)[U]) {
-    in_t ra[U], rb[U];
-    acc_t xa[U], xb[U];
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       if (vv[j] >= 0) {
         if constexpr (kSameVec) {
-          xa[j] = ldg<acc_t, NT, kA>(e(j).own + off<acc_t>(vv[j], st.V, st.back));
-          xb[j] = ldg<acc_t, NT, kA>(e(j).child + off<acc_t>(vv[j], st.V, st.back));
+          xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
+          xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
         } else {
-          if (e(j).own_in)
-            ra[j] = ldg<in_t, NT, kA>(e(j).own + off<in_t>(vv[j], st.V, st.back));
+          if (e[j].own_in)
+            ra[j] = ldg<in_t, NT, kA>(e[j].own + off<in_t>(vv[j], st.V, st.back));
           else
-            xa[j] = ldg<acc_t, NT, kA>(e(j).own + off<acc_t>(vv[j], st.V, st.back));
-          if (e(j).child_in)
-            rb[j] = ldg<in_t, NT, kA>(e(j).child + off<in_t>(vv[j], st.V, st.back));
+            xa[j] = ldg<acc_t, NT, kA>(e[j].own + off<acc_t>(vv[j], st.V, st.back));
+          if (e[j].child_in)
+            rb[j] = ldg<in_t, NT, kA>(e[j].child + off<in_t>(vv[j], st.V, st.back));
           else
-            xb[j] = ldg<acc_t, NT, kA>(e(j).child + off<acc_t>(vv[j], st.V, st.back));
+            xb[j] = ldg<acc_t, NT, kA>(e[j].child + off<acc_t>(vv[j], st.V, st.back));
         }
       }
     }
@@ -826,15 +814,15 @@ struct RsOp {
       if (vv[j] >= 0) {
         acc_t a = xa[j], b = xb[j];
         if constexpr (!kSameVec) {
-          if (e(j).own_in) a = R::widen(ra[j]);
-          if (e(j).child_in) b = R::widen(rb[j]);
+          if (e[j].own_in) a = R::widen(ra[j]);
+          if (e[j].child_in) b = R::widen(rb[j]);
         }
         sum[j] = R::add(a, b);
       }
     wait_loads();
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      if (vv[j] >= 0) store(e(j), vv[j], st.V, st.back, sum[j]);
+      if (vv[j] >= 0) store(e[j], vv[j], st.V, st.back, sum[j]);
   }
 
   // Every edge of step st in tree c, over vectors [t0, t0 + TV) of the chunk;
