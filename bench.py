@@ -804,7 +804,8 @@ def main():
     ap.add_argument("--aggregation", default="pow2", choices=["pow2", "budget"],
                     help="with --budget-sweep: power-of-two sub-trees, or any chunks per step (list schedule)")
     ap.add_argument("--misalign-probe", action="store_true",
-                    help="instead: 256-byte chunk copies at a skew, one launch or even/odd chunks in two")
+                    help="instead: 256-byte chunk copies at a skew, one launch or even/odd chunks in two, and "
+                         "the N=1000 all-gather aligned, one element off and with an odd count")
     ap.add_argument("--step-clock", action="store_true",
                     help="instead: per-step device clock of the workload's fused launch (PAT_STEP_CLOCK=1)")
     ap.add_argument("--size-sweep", action="store_true",
