@@ -62,9 +62,10 @@ int oracle_allgather(const void* inputs, int kind, uint64_t seed, int64_t lo, ui
   if (nranks < 1 || count < 0 || dtype < kInt32 || dtype > kBfloat16 || !out) return -1;
   if (r0 < 0 || r1 > nranks || r0 > r1) return -1;
   if (!inputs && (kind < 0 || kind > 3 || (kind >= 2 && !table))) return -1;
+  if (threads <= 0) threads = cpus();
+  if (count == 0 || r0 == r1) return 1;  // nothing to copy
   const size_t esize = dtype == kBfloat16 ? 2 : 4;
   const size_t chunk = size_t(count) * esize;
-  if (threads <= 0) threads = cpus();
   // A work item: a run of `per` consecutive chunks of one receiver's row,
   // about 64 KiB.
   const int64_t per = std::max<int64_t>(1, std::min<int64_t>(nranks, int64_t(65536) / int64_t(std::max<size_t>(chunk, 1))));

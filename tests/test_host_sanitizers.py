@@ -1,6 +1,8 @@
-"""The host plan code under AddressSanitizer and UndefinedBehaviorSanitizer
-(g++, host code only): the plan code driven over many plans by tests/host/plan_check.cpp,
-and the C-ABI layer against launch stubs driven by tests/host/api_check.cpp."""
+"""Host code under AddressSanitizer and UndefinedBehaviorSanitizer (g++, host
+code only): the plan code driven over many plans by tests/host/plan_check.cpp,
+the C-ABI layer against launch stubs driven by tests/host/api_check.cpp, and
+the threaded C++ oracle (also under ThreadSanitizer) driven by
+tests/host/oracle_check.cpp."""
 
 import os
 import shutil
@@ -46,3 +48,21 @@ def test_abi_host_paths_under_asan_ubsan(tmp_path):
                          env=dict(os.environ, ASAN_OPTIONS="detect_leaks=0"))
     assert res.returncode == 0, (res.stdout[-1000:], res.stderr[-2000:])
     assert "plans checked, 0 failures" in res.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="no g++")
+@pytest.mark.parametrize("sanitizer", ["address,undefined", "thread"])
+def test_threaded_oracle_under_sanitizers(tmp_path, sanitizer):
+    """The threaded C++ oracle (reduce-scatter and all-gather) driven by
+    tests/host/oracle_check.cpp over every generator kind and dtype, ranks
+    1 .. 100, empty and ragged counts, ranges and thread counts, under
+    AddressSanitizer + UndefinedBehaviorSanitizer and under ThreadSanitizer."""
+    exe = tmp_path / "oracle_check"
+    oracle = os.path.join(ROOT, "oracle")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-pthread", f"-fsanitize={sanitizer}", "-fno-sanitize-recover=all",
+           "-ffp-contract=off", "-I", ROOT, os.path.join(oracle, "rs_oracle.cpp"), os.path.join(oracle, "ag_oracle.cpp"),
+           os.path.join(ROOT, "tests", "host", "oracle_check.cpp"), "-o", str(exe)]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True, timeout=600)
+    assert res.returncode == 0, (res.stdout[-1000:], res.stderr[-3000:])
+    assert "oracle cases checked, 0 failures" in res.stdout
